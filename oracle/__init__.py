@@ -1,0 +1,23 @@
+"""CPU oracle for the blockwise FP8 W8A8 linear layer -- TEST INFRASTRUCTURE ONLY.
+
+This package is a plain, slow, obviously-correct restatement of what the paper
+("FP8-RL", arXiv 2601.18150) computes on its FP8 linear-layer hot path:
+
+* ``e4m3``  -- the OCP E4M3 ("fn") codec, from the format definition
+  (section 2.1.1: 4 exponent bits, 3 mantissa bits, range about +-448;
+  section 3.1 / ref. [12] for the encoding family).
+* ``quant`` -- blockwise weight quantisation with one fp32 scale per
+  128x128 block (section 2.1.1, Eq. (1)) and dynamic per-token activation
+  quantisation with one fp32 scale per 1x128 group (section 2.1.1 "Static vs
+  dynamic quantization", section 3.1 "1x128 tiles for activations").
+* ``gemm``  -- the blockwise-scaled FP8 GEMM, dense and grouped by expert
+  (section 2.1.4 / section 2.1.1 quantisation scope incl. MoE fc1/fc2),
+  evaluated as dequantise-then-matmul in fp64.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import, call or execute anything in this package.  The HIP
+product path never does; it shares no code, table or constant generator with
+this package.  Everything here is numpy on the CPU (plus one small C file,
+``e4m3_sweep.c``, used only by the exhaustive element-map test).
+"""
+from . import e4m3, quant, gemm  # noqa: F401
