@@ -1,0 +1,276 @@
+"""Benchmark of the blockwise FP8 W8A8 linear-layer hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+  1. weight re-quantisation   bf16 W [N][K] -> E4M3 + 128x128 fp32 block scales
+  2. activation quantisation  bf16 A [M][K] -> E4M3 + 1x128 fp32 group scales
+  3. blockwise FP8 GEMM       Y [M][N] bf16
+on the Qwen3-8B-shaped prefill gate_up linear (M=8192 tokens, K=4096, N=24576),
+with 1% outlier activation channels (x50) and 0.1% outlier weights (x20).
+
+The JSON line's `value` is the step's effective GEMM throughput (2MNK per step
+/ step time, TFLOP/s, all three kernels inside the timed region).  `roofline`
+is the GEMM kernel alone, timed with HIP events on the stream it runs on.
+`extra` carries the same run's weight-resync figure (36 Qwen3-8B layers, 144
+matrices, GB/s vs HBM) and the MoE grouped GEMM (Qwen3-30B-A3B experts).
+`cpu_baseline` times the CPU oracle on a bounded row sample of the same step.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload prefill]
+                       [--no-cpu-baseline] [--no-extra]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP8_PEAK_TFLOPS = 5000.0       # MI355X dense FP8 MFMA, TFLOP/s
+METRIC = "blockwise FP8 GEMM TFLOP/s (% FP8 MFMA peak); weight requant GB/s (% HBM)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true")
+    ap.add_argument("--seed", type=int, default=3)
+    return ap.parse_args()
+
+
+class KernelTimer:
+    """HIP events around individual launches on the current stream; averages per name."""
+
+    def __init__(self):
+        self.pending = []
+        self.on = False
+
+    def span(self, name):
+        timer = self
+
+        class _S:
+            def __enter__(self):
+                if timer.on:
+                    self.e0 = torch.cuda.Event(enable_timing=True)
+                    self.e1 = torch.cuda.Event(enable_timing=True)
+                    self.e0.record()
+
+            def __exit__(self, *a):
+                if timer.on:
+                    self.e1.record()
+                    timer.pending.append((name, self.e0, self.e1))
+        return _S()
+
+    def averages_ms(self):
+        torch.cuda.synchronize()
+        acc = {}
+        for name, e0, e1 in self.pending:
+            acc.setdefault(name, []).append(e0.elapsed_time(e1))
+        return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def timed_loop(step, steps, warmup, timer):
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    timer.on = True
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    timer.on = False
+    return start.elapsed_time(stop) / steps, wall
+
+
+# ---------------------------------------------------------------------------
+# prefill step (the headline workload)
+# ---------------------------------------------------------------------------
+def prefill(args, fp8rl):
+    m, k, n = 8192, 4096, 24576
+    a, w = synth.prefill_linear(seed=args.seed, device="cuda", m=m, k=k, n=n)
+    qw = torch.empty((n, k), dtype=torch.uint8, device="cuda")
+    sw = torch.empty((n // 128, k // 128), dtype=torch.float32, device="cuda")
+    qa = torch.empty((m, k), dtype=torch.uint8, device="cuda")
+    sa = torch.empty((k // 128, m), dtype=torch.float32, device="cuda")
+    y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+    timer = KernelTimer()
+
+    def step():
+        with timer.span("quant_weight"):
+            fp8rl.fp8rl_quant_weight_block128(w, q=qw, scale=sw)
+        with timer.span("quant_act"):
+            fp8rl.fp8rl_quant_act_token_group128(a, q=qa, scale=sa)
+        with timer.span("gemm"):
+            fp8rl.fp8rl_gemm_w8a8_block(qa, sa, qw, sw, y=y)
+
+    ms, wall = timed_loop(step, args.steps, args.warmup, timer)
+    kern = timer.averages_ms()
+    flops = 2.0 * m * n * k
+    gemm_tflops = flops / (kern["gemm"] * 1e-3) / 1e12
+    qw_bytes = n * k * 2 + n * k + (n // 128) * (k // 128) * 4
+    qa_bytes = m * k * 2 + m * k + (k // 128) * m * 4
+    out = {
+        "metric": METRIC,
+        "value": round(flops / (ms * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "ms_per_step": round(ms, 4),
+        "wall_s_timed": round(wall, 3),
+        "dtype": "fp8e4m3 x fp8e4m3 -> fp32 acc -> bf16",
+        "config": {"workload": "Qwen3-8B prefill gate_up linear: weight requant + activation quant + "
+                               "blockwise FP8 GEMM", "M": m, "K": k, "N": n,
+                   "weight_block": [128, 128], "act_group": [1, 128], "seed": args.seed},
+        "roofline": {
+            "bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": None,
+            "kernel": "gemm_w8a8_block", "avg_ms": round(kern["gemm"], 5),
+            "algorithmic_flops_per_launch": flops,
+        },
+        "kernels": {
+            "quant_weight_block128": {"avg_ms": round(kern["quant_weight"], 5),
+                                      "GB/s": round(qw_bytes / (kern["quant_weight"] * 1e-3) / 1e9, 1)},
+            "quant_act_token_group128": {"avg_ms": round(kern["quant_act"], 5),
+                                         "GB/s": round(qa_bytes / (kern["quant_act"] * 1e-3) / 1e9, 1)},
+            "gemm_w8a8_block": {"avg_ms": round(kern["gemm"], 5), "TFLOP/s": round(gemm_tflops, 1)},
+        },
+    }
+    return out, (a, w)
+
+
+# ---------------------------------------------------------------------------
+# weight resync: 36 layers x 4 matrices
+# ---------------------------------------------------------------------------
+def requant(args, fp8rl, steps=3, warmup=1):
+    mats = []
+    for layer in range(synth.QWEN3_8B_LAYERS):
+        for name in synth.QWEN3_8B_LINEARS:
+            w, _, _ = synth.requant_matrix(layer, name, device="cuda")
+            n, k = w.shape
+            mats.append((w, torch.empty((n, k), dtype=torch.uint8, device="cuda"),
+                         torch.empty((n // 128, k // 128), dtype=torch.float32, device="cuda")))
+    elems = sum(w.numel() for w, _, _ in mats)
+    nbytes = sum(w.numel() * 3 + s.numel() * 4 for w, _, s in mats)
+    timer = KernelTimer()
+
+    def step():
+        for w, q, s in mats:
+            with timer.span("quant_weight"):
+                fp8rl.fp8rl_quant_weight_block128(w, q=q, scale=s)
+
+    ms, _ = timed_loop(step, steps, warmup, timer)
+    kern_ms = timer.averages_ms()["quant_weight"]
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    del mats
+    torch.cuda.empty_cache()
+    return {"workload": "weight resync, 36 Qwen3-8B layers x {qkv, o_proj, gate_up, down}, 144 launches",
+            "elements": elems, "bytes": nbytes, "ms_per_pass": round(ms, 4),
+            "GB/s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+            "sum_kernel_ms": round(kern_ms * len(timer.pending) / max(1, steps), 4)}
+
+
+# ---------------------------------------------------------------------------
+# MoE grouped GEMM (gate_up and down)
+# ---------------------------------------------------------------------------
+def moe(args, fp8rl, steps=10, warmup=3):
+    lay = synth.moe_layer(device="cuda")
+    off = lay["routing"].offsets.to("cuda")
+    counts = lay["routing"].counts
+    res = {}
+    for which in ("gate_up", "down"):
+        x = lay["x_gate_up"] if which == "gate_up" else lay["x_down"]
+        wts = lay["w_gate_up"] if which == "gate_up" else lay["w_down"]
+        g, n, k = wts.shape
+        qw, sw = fp8rl.fp8rl_quant_weight_block128(wts.reshape(g * n, k))
+        qw = qw.reshape(g, n, k)
+        sw = sw.reshape(g, n // 128, k // 128)
+        qa, sa = fp8rl.fp8rl_quant_act_token_group128(x)
+        y = torch.empty((x.shape[0], n), dtype=torch.bfloat16, device="cuda")
+        timer = KernelTimer()
+
+        def step():
+            with timer.span("grouped"):
+                fp8rl.fp8rl_grouped_gemm_w8a8_block(qa, sa, qw, sw, off, y=y)
+
+        timed_loop(step, steps, warmup, timer)
+        kms = timer.averages_ms()["grouped"]
+        rows = x.shape[0]
+        flops = 2.0 * rows * n * k
+        active = int((counts > 0).sum())
+        nbytes = active * n * k + rows * k + rows * n * 2 + rows * (k // 128) * 4
+        t = flops / (kms * 1e-3) / 1e12
+        res[which] = {"N": n, "K": k, "rows": rows, "active_experts": active, "avg_ms": round(kms, 5),
+                      "TFLOP/s": round(t, 1), "frac_fp8_peak": round(t / FP8_PEAK_TFLOPS, 4),
+                      "GB/s_min_traffic": round(nbytes / (kms * 1e-3) / 1e9, 1)}
+    del lay
+    torch.cuda.empty_cache()
+    return res
+
+
+# ---------------------------------------------------------------------------
+# CPU oracle baseline on a bounded sample of the prefill step
+# ---------------------------------------------------------------------------
+def cpu_baseline(a, w, rows=16):
+    import numpy as np
+    from oracle import gemm, quant
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    a_s = a[:rows].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    w_h = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    t0 = time.perf_counter()
+    qw, sw = quant.quant_weight_block128(w_h)
+    qa, sa = quant.quant_act_token_group128(a_s)
+    gemm.gemm_ref_fp64(qa, sa, qw, sw)
+    dt = time.perf_counter() - t0
+    m, k = a.shape
+    n = w.shape[0]
+    flops = 2.0 * rows * n * k
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} of {m} token rows through the full step (weight quantisation of "
+                      f"all {n}x{k} weights, activation quantisation, fp64 GEMM); {dt:.1f} s on the host",
+            "seconds": round(dt, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; multi-GPU runs are not part of it",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import paper_2601_18150_amd as fp8rl
+    fp8rl.load()
+    torch.cuda.init()
+    if args.workload != "prefill":
+        fn = {"requant": requant, "moe": moe}.get(args.workload)
+        if fn is None:
+            raise SystemExit("decode workload: see the parity tests")
+        print(json.dumps(fn(args, fp8rl)), flush=True)
+        return
+    out, (a, w) = prefill(args, fp8rl)
+    out.update({"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
+                "scaling": "weak", "vs_baseline": None, "data": "synthetic"})
+    if not args.no_extra:
+        extra = {"weight_resync": requant(args, fp8rl), "moe_grouped": moe(args, fp8rl)}
+        out["extra"] = extra
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(a, w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,148 @@
+/*
+ * fp8rl -- blockwise FP8 (OCP E4M3) W8A8 linear layer for AMD MI355X (gfx950).
+ *
+ * The operations follow the FP8 rollout method of "FP8-RL" (arXiv 2601.18150):
+ *   - weights are quantised to E4M3 with one fp32 scale per 128x128 block,
+ *     re-run after every RL step when the trainer's bf16 weights are synced
+ *     into the rollout engine (section 2.1.1, Eq. (1); section 2.1.2);
+ *   - activations are quantised dynamically at every forward pass with one
+ *     fp32 scale per token and 128-wide group along K (section 2.1.1 "Static vs
+ *     dynamic quantization"; section 3.1 "1x128 tiles for activations");
+ *   - the linear layer is an FP8 GEMM consuming both, accumulating in fp32 and
+ *     writing bf16, dense or grouped per MoE expert (section 2.1.1
+ *     "Quantization scope", section 2.1.4).
+ *
+ * Conventions shared by every entry point
+ *   - All data pointers are DEVICE pointers (memory of the current HIP device)
+ *     owned by the caller.  The library allocates no memory, never
+ *     synchronises, keeps no state between calls, and only enqueues kernels on
+ *     `stream` (a hipStream_t; NULL = the default stream).  Calls are
+ *     asynchronous: a device fault surfaces at the caller's next sync.
+ *   - bf16 values are passed as their uint16_t bit patterns, E4M3 values as
+ *     uint8_t codes (OCP E4M3 "fn": bias 7, max 448, 0x7F/0xFF NaN, no inf).
+ *   - Matrices are row-major; ld* is the distance in ELEMENTS between rows.
+ *   - Outputs must not alias inputs.
+ *   - Return value: FP8RL_OK or an error code.  On any error nothing is
+ *     launched and no output is touched.
+ *   - Size 0 along M (or total_rows) is a valid no-op returning FP8RL_OK.
+ *   - Inputs must be finite (no NaN/inf); for non-finite inputs the outputs are
+ *     unspecified (not checked: it would need a device read).
+ *
+ * Quantisation rule (identical for weight blocks and activation groups):
+ *   amax  = max |x| over the block/group (bf16 widened exactly to fp32)
+ *   scale = amax / 448 as an IEEE fp32 division (round to nearest even,
+ *           subnormals kept); scale = 1.0 when amax == 0
+ *   code  = E4M3(fl32(x / scale)) -- one IEEE fp32 division, then one
+ *           round-to-nearest-even onto the E4M3 grid, saturating at +-448,
+ *           keeping the sign of x (so -0 gives 0x80).
+ *   Every block/group's largest element therefore maps to +-448 exactly.
+ *   Codes and scales are bit-for-bit deterministic.
+ */
+#ifndef FP8RL_H
+#define FP8RL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FP8RL_OK = 0,
+  FP8RL_ERR_INVALID_ARG = 1,       /* null pointer with nonzero size, negative size, ld too small, num_groups < 1 */
+  FP8RL_ERR_UNSUPPORTED_SHAPE = 2, /* K or N not a multiple of 128, or a size beyond 2^31 elements per row/col */
+  FP8RL_ERR_MISALIGNED = 3,        /* a pointer or leading dimension breaks the alignment rules stated below */
+  FP8RL_ERR_HIP = 4                /* the HIP runtime reported an error at launch */
+} fp8rl_status;
+
+/*
+ * Weight quantisation, one fp32 scale per 128x128 block (section 2.1.1, Eq. (1)).
+ *
+ * w      [n][ldw]  bf16 weight, nn.Linear layout: n output rows, k input columns
+ * q      [n][ldq]  E4M3 codes out
+ * scale  [n/128][k/128] fp32 out, contiguous; scale[i*(k/128)+j] belongs to
+ *        rows 128i..128i+127, columns 128j..128j+127
+ * n, k   multiples of 128 (else FP8RL_ERR_UNSUPPORTED_SHAPE); n == 0 is a no-op
+ * Alignment: w, q 16-byte aligned; ldw % 8 == 0; ldq % 16 == 0; scale 4-byte aligned.
+ * ldw >= k, ldq >= k (else FP8RL_ERR_INVALID_ARG).
+ */
+int fp8rl_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
+                                uint8_t* q, int64_t ldq, float* scale, void* stream);
+
+/*
+ * Dynamic activation quantisation, one fp32 scale per token per 128-wide K group
+ * (section 2.1.1 "Static vs dynamic quantization"; section 3.1 1x128 tiles).
+ *
+ * a      [m][lda]  bf16 activations (m tokens, k features)
+ * q      [m][ldq]  E4M3 codes out
+ * scale  [k/128][ld_scale] fp32 out, token index contiguous:
+ *        scale[g*ld_scale + t] belongs to token t, columns 128g..128g+127.
+ *        Entries t >= m are not written.
+ * k      multiple of 128; m >= 0 arbitrary (m == 0 is a no-op)
+ * Alignment: a, q 16-byte aligned; lda % 8 == 0; ldq % 16 == 0; scale 4-byte aligned.
+ * lda >= k, ldq >= k, ld_scale >= m.
+ */
+int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
+                                   uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
+                                   void* stream);
+
+/*
+ * Dense blockwise-scaled FP8 GEMM:  y = bf16( qa . qw^T ) with the block scales
+ * (section 2.1.1 Eq. (1) scales on both operands; section 2.1.4 FP8 GEMM):
+ *
+ *   y[i][j] = bf16_rne( sum_kb  sa[kb*ld_sa + i] * sw[(j/128)*(k/128) + kb]
+ *                               * sum_{c in kb} dec(qa[i][c]) * dec(qw[j][c]) )
+ *
+ * qa  [m][lda] E4M3 activation codes; sa [k/128][ld_sa] their scales (as written
+ *     by fp8rl_quant_act_token_group128)
+ * qw  [n][ldw] E4M3 weight codes;     sw [n/128][k/128] their block scales (as
+ *     written by fp8rl_quant_weight_block128)
+ * y   [m][ldy] bf16 out
+ * fp32 accumulation inside each 128-wide K block, fp32 scale application per K
+ * block, fp32 -> bf16 round-to-nearest-even at the end; no bias.
+ * n, k multiples of 128; m >= 0 arbitrary (m == 0 is a no-op).
+ * Alignment: qa, qw, y 16-byte aligned; lda % 16 == 0; ldw % 16 == 0; ldy % 8 == 0;
+ * sa, sw 4-byte aligned.  lda >= k, ldw >= k, ldy >= n, ld_sa >= m.
+ */
+int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                          const uint8_t* qw, int64_t ldw, const float* sw,
+                          uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,
+                          void* stream);
+
+/*
+ * Grouped (MoE expert) blockwise-scaled FP8 GEMM (section 2.1.1: MoE expert
+ * layers fc1/fc2 are quantised like every other linear layer).
+ *
+ * Rows are stored grouped by expert: rows group_offsets[e] .. group_offsets[e+1]-1
+ * of qa / y belong to expert e and use weight e.  For each expert with rows:
+ *   y[rows of e] = the dense product above with qw[e], sw[e].
+ * Experts without rows cost nothing and write nothing.
+ *
+ * qa            [total_rows][k] E4M3 codes, contiguous
+ * sa            [k/128][ld_sa] fp32, indexed by global row; ld_sa >= total_rows
+ * qw            [num_groups][n][k] E4M3 codes, contiguous
+ * sw            [num_groups][n/128][k/128] fp32, contiguous
+ * group_offsets DEVICE int32 [num_groups+1]: offsets[0] == 0, non-decreasing,
+ *               offsets[num_groups] == total_rows (precondition, not checked:
+ *               checking would need a device read)
+ * y             [total_rows][n] bf16 out, contiguous
+ * n, k multiples of 128; num_groups >= 1; total_rows >= 0 (0 is a no-op).
+ * Alignment: qa, qw, y 16-byte aligned; k % 16 == 0 follows from k % 128 == 0.
+ */
+int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,
+                                  const uint8_t* qw, const float* sw,
+                                  const int32_t* group_offsets, int64_t num_groups,
+                                  int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
+                                  void* stream);
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* fp8rl_status_string(int status);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int fp8rl_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FP8RL_H */

@@ -1,0 +1,258 @@
+"""Python binding of libfp8rl -- blockwise FP8 (E4M3) W8A8 linear layer on MI355X.
+
+Argument marshalling only: every function below checks tensor shapes, dtypes
+and devices, allocates outputs with torch when they are not supplied, and
+calls the C entry point of the same name (include/fp8rl.h) on the current
+torch stream.  All arithmetic runs in the HIP kernels of libfp8rl.so; there is
+no CPU fallback: the library is loaded on first use (or by ``load()``) and a
+missing or unloadable library raises ImportError.
+
+Paper: "FP8-RL", arXiv 2601.18150 -- section 2.1.1 (blockwise E4M3 weights with
+128x128 fp32 block scales, Eq. (1); dynamic per-token 1x128 activation
+scales), section 2.1.2 (weights re-quantised at every RL step), section 2.1.4
+(FP8 GEMM for the W8A8 linear layers, dense and MoE experts).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # loads torch's HIP runtime first, so libfp8rl binds to that same runtime
+
+__all__ = [
+    "LIB_PATH", "Fp8rlError", "load",
+    "fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
+    "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
+    "fp8rl_status_string", "fp8rl_version",
+    "quant_weight_block128", "quant_act_token_group128", "gemm_w8a8_block",
+    "grouped_gemm_w8a8_block", "linear_w8a8",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfp8rl.so")
+
+_STATUS = {0: "FP8RL_OK", 1: "FP8RL_ERR_INVALID_ARG", 2: "FP8RL_ERR_UNSUPPORTED_SHAPE",
+           3: "FP8RL_ERR_MISALIGNED", 4: "FP8RL_ERR_HIP"}
+
+
+class Fp8rlError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} returned {status} ({_STATUS.get(status, 'unknown')})")
+        self.status = status
+
+
+def _hip_runtimes_mapped():
+    try:
+        with open("/proc/self/maps") as f:
+            paths = {ln.split()[-1] for ln in f if "libamdhip64" in ln}
+        return sorted(p for p in paths if p.startswith("/"))
+    except OSError:
+        return []
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2601_18150_amd.build` "
+                          "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I = ctypes.c_void_p, ctypes.c_int64
+    sig = {
+        "fp8rl_quant_weight_block128": [P, I, I, I, P, I, P, P],
+        "fp8rl_quant_act_token_group128": [P, I, I, I, P, I, P, I, P],
+        "fp8rl_gemm_w8a8_block": [P, I, P, I, P, I, P, P, I, I, I, I, P],
+        "fp8rl_grouped_gemm_w8a8_block": [P, P, I, P, P, P, I, I, P, I, I, P],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    lib.fp8rl_status_string.argtypes = [ctypes.c_int]
+    lib.fp8rl_status_string.restype = ctypes.c_char_p
+    lib.fp8rl_version.argtypes = []
+    lib.fp8rl_version.restype = ctypes.c_int
+    runtimes = _hip_runtimes_mapped()
+    if len(runtimes) > 1:
+        raise ImportError(f"two HIP runtimes mapped in this process: {runtimes}")
+    return lib
+
+
+_lib = None
+
+
+def load():
+    """Load libfp8rl.so (once) and return the ctypes handle."""
+    global _lib
+    if _lib is None:
+        _lib = _load()
+    return _lib
+
+
+def _check(name: str, status: int):
+    if status != 0:
+        raise Fp8rlError(name, status)
+
+
+def _stream(stream=None) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _dev(*ts):
+    dev = None
+    for t in ts:
+        if not t.is_cuda:
+            raise ValueError("fp8rl tensors must live on a HIP device")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError("fp8rl tensors must share one device")
+    return dev
+
+
+def _ld(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a 2-D row-major tensor with unit column stride")
+    return t.stride(0) if t.size(0) > 1 else max(t.stride(0), t.size(1))
+
+
+def _u8(t: torch.Tensor) -> torch.Tensor:
+    if t.dtype == torch.uint8:
+        return t
+    if t.dtype == torch.float8_e4m3fn:
+        return t.view(torch.uint8)
+    raise TypeError(f"expected uint8 / float8_e4m3fn codes, got {t.dtype}")
+
+
+# ---------------------------------------------------------------------------
+# Entry points with the C names
+# ---------------------------------------------------------------------------
+def fp8rl_status_string(status: int) -> str:
+    return load().fp8rl_status_string(int(status)).decode()
+
+
+def fp8rl_version() -> int:
+    return int(load().fp8rl_version())
+
+
+def fp8rl_quant_weight_block128(w: torch.Tensor, q: torch.Tensor | None = None,
+                                scale: torch.Tensor | None = None, stream=None):
+    """bf16 weight [N][K] -> (E4M3 codes uint8 [N][K], fp32 scales [N/128][K/128])."""
+    if w.dtype != torch.bfloat16 or w.dim() != 2:
+        raise TypeError("w must be a 2-D bfloat16 tensor")
+    n, k = w.shape
+    if q is None:
+        q = torch.empty((n, k), dtype=torch.uint8, device=w.device)
+    if scale is None:
+        scale = torch.empty((n // 128, k // 128), dtype=torch.float32, device=w.device)
+    q = _u8(q)
+    _dev(w, q, scale)
+    if scale.dtype != torch.float32 or not scale.is_contiguous() or scale.numel() < (n // 128) * (k // 128):
+        raise ValueError("scale must be a contiguous fp32 tensor of [N/128][K/128] elements")
+    st = load().fp8rl_quant_weight_block128(w.data_ptr(), n, k, _ld(w), q.data_ptr(), _ld(q),
+                                         scale.data_ptr(), _stream(stream))
+    _check("fp8rl_quant_weight_block128", st)
+    return q, scale
+
+
+def fp8rl_quant_act_token_group128(a: torch.Tensor, q: torch.Tensor | None = None,
+                                   scale: torch.Tensor | None = None, ld_scale: int | None = None,
+                                   stream=None):
+    """bf16 activations [M][K] -> (E4M3 codes uint8 [M][K], fp32 scales [K/128][ld_scale])."""
+    if a.dtype != torch.bfloat16 or a.dim() != 2:
+        raise TypeError("a must be a 2-D bfloat16 tensor")
+    m, k = a.shape
+    if scale is not None and ld_scale is None:
+        ld_scale = scale.stride(0) if scale.dim() == 2 else m
+    if ld_scale is None:
+        ld_scale = m
+    if q is None:
+        q = torch.empty((m, k), dtype=torch.uint8, device=a.device)
+    if scale is None:
+        scale = torch.empty((k // 128, ld_scale), dtype=torch.float32, device=a.device)
+    q = _u8(q)
+    _dev(a, q, scale)
+    if scale.dtype != torch.float32 or scale.numel() < (k // 128) * ld_scale and m > 0:
+        raise ValueError("scale must be fp32 with at least [K/128][ld_scale] elements")
+    st = load().fp8rl_quant_act_token_group128(a.data_ptr(), m, k, _ld(a) if m else k, q.data_ptr(),
+                                            _ld(q) if m else k, scale.data_ptr(), ld_scale, _stream(stream))
+    _check("fp8rl_quant_act_token_group128", st)
+    return q, scale
+
+
+def fp8rl_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
+                          y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """y[M][N] bf16 = blockwise-scaled FP8 product of qa [M][K] (scales sa [K/128][>=M])
+    and qw [N][K] (scales sw [N/128][K/128])."""
+    qa, qw = _u8(qa), _u8(qw)
+    m, k = qa.shape
+    n, k2 = qw.shape
+    if k != k2:
+        raise ValueError("K mismatch")
+    if sa.dtype != torch.float32 or sw.dtype != torch.float32:
+        raise TypeError("scales must be fp32")
+    if sa.dim() != 2 or sa.size(0) != k // 128 or sa.stride(1) != 1 or sa.size(1) < m:
+        raise ValueError("sa must be [K/128][ld >= M] with unit stride")
+    if not sw.is_contiguous() or sw.numel() != (n // 128) * (k // 128):
+        raise ValueError("sw must be contiguous [N/128][K/128]")
+    if y is None:
+        y = torch.empty((m, n), dtype=torch.bfloat16, device=qa.device)
+    if y.dtype != torch.bfloat16 or tuple(y.shape) != (m, n):
+        raise ValueError("y must be bf16 [M][N]")
+    _dev(qa, sa, qw, sw, y)
+    if m == 0:
+        return y
+    st = load().fp8rl_gemm_w8a8_block(qa.data_ptr(), _ld(qa), sa.data_ptr(), sa.stride(0), qw.data_ptr(),
+                                   _ld(qw), sw.data_ptr(), y.data_ptr(), _ld(y), m, n, k, _stream(stream))
+    _check("fp8rl_gemm_w8a8_block", st)
+    return y
+
+
+def fp8rl_grouped_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
+                                  group_offsets: torch.Tensor, y: torch.Tensor | None = None,
+                                  stream=None) -> torch.Tensor:
+    """Per expert e: y[off_e:off_e+1] = blockwise FP8 product with qw[e], sw[e].
+
+    qa [R][K] codes grouped by expert; sa [K/128][ld >= R]; qw [G][N][K];
+    sw [G][N/128][K/128]; group_offsets int32 [G+1] on the device.
+    """
+    qa, qw = _u8(qa), _u8(qw)
+    r, k = qa.shape
+    g, n, k2 = qw.shape
+    if k != k2:
+        raise ValueError("K mismatch")
+    if not qa.is_contiguous() or not qw.is_contiguous() or not sw.is_contiguous():
+        raise ValueError("qa, qw and sw must be contiguous")
+    if sw.numel() != g * (n // 128) * (k // 128) or sw.dtype != torch.float32:
+        raise ValueError("sw must be fp32 [G][N/128][K/128]")
+    if sa.dtype != torch.float32 or sa.dim() != 2 or sa.size(0) != k // 128 or sa.stride(1) != 1 or sa.size(1) < r:
+        raise ValueError("sa must be fp32 [K/128][ld >= R]")
+    if group_offsets.dtype != torch.int32 or group_offsets.numel() != g + 1 or not group_offsets.is_contiguous():
+        raise ValueError("group_offsets must be a contiguous int32 tensor of G+1 entries")
+    if y is None:
+        y = torch.empty((r, n), dtype=torch.bfloat16, device=qa.device)
+    if y.dtype != torch.bfloat16 or tuple(y.shape) != (r, n) or not y.is_contiguous():
+        raise ValueError("y must be contiguous bf16 [R][N]")
+    _dev(qa, sa, qw, sw, group_offsets, y)
+    if r == 0:
+        return y
+    st = load().fp8rl_grouped_gemm_w8a8_block(qa.data_ptr(), sa.data_ptr(), sa.stride(0), qw.data_ptr(),
+                                           sw.data_ptr(), group_offsets.data_ptr(), g, r, y.data_ptr(),
+                                           n, k, _stream(stream))
+    _check("fp8rl_grouped_gemm_w8a8_block", st)
+    return y
+
+
+# short aliases
+quant_weight_block128 = fp8rl_quant_weight_block128
+quant_act_token_group128 = fp8rl_quant_act_token_group128
+gemm_w8a8_block = fp8rl_gemm_w8a8_block
+grouped_gemm_w8a8_block = fp8rl_grouped_gemm_w8a8_block
+
+
+def linear_w8a8(x: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor, stream=None) -> torch.Tensor:
+    """The W8A8 linear layer's forward: dynamic activation quantisation, then the
+    blockwise FP8 GEMM, both on one stream with no host synchronisation."""
+    qa, sa = fp8rl_quant_act_token_group128(x, stream=stream)
+    return fp8rl_gemm_w8a8_block(qa, sa, qw, sw, stream=stream)

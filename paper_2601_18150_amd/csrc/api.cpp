@@ -1,0 +1,102 @@
+// C ABI of libfp8rl (declared in include/fp8rl.h): argument validation, then
+// one launch on the caller's stream.  No allocation, no synchronisation, no
+// state kept between calls.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/fp8rl.h"
+#include "launch.hpp"
+
+namespace {
+
+constexpr int64_t kMaxDim = int64_t(1) << 31;   // per-dimension limit (32-bit tile indices)
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? FP8RL_OK : FP8RL_ERR_HIP; }
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+const char* fp8rl_status_string(int status) {
+  switch (status) {
+    case FP8RL_OK: return "FP8RL_OK";
+    case FP8RL_ERR_INVALID_ARG: return "FP8RL_ERR_INVALID_ARG";
+    case FP8RL_ERR_UNSUPPORTED_SHAPE: return "FP8RL_ERR_UNSUPPORTED_SHAPE";
+    case FP8RL_ERR_MISALIGNED: return "FP8RL_ERR_MISALIGNED";
+    case FP8RL_ERR_HIP: return "FP8RL_ERR_HIP";
+    default: return "FP8RL_ERR_UNKNOWN";
+  }
+}
+
+int fp8rl_version(void) { return 100; }   // 0.1.0
+
+int fp8rl_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q,
+                                int64_t ldq, float* scale, void* stream) {
+  if (n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
+  if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (n >= kMaxDim || k >= kMaxDim || (n / 128) * (k / 128) >= (int64_t(1) << 24))
+    return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (n == 0 || k == 0) return FP8RL_OK;
+  if (!w || !q || !scale) return FP8RL_ERR_INVALID_ARG;
+  if (ldw < k || ldq < k) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(w, 16) || !aligned(q, 16) || !aligned(scale, 4) || ldw % 8 || ldq % 16)
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_quant_weight_block128(w, n, k, ldw, q, ldq, scale, as_stream(stream)));
+}
+
+int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda, uint8_t* q,
+                                   int64_t ldq, float* scale, int64_t ld_scale, void* stream) {
+  if (m < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
+  if (k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m >= kMaxDim || k >= kMaxDim || m * (k / 128) >= (int64_t(1) << 28)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m == 0 || k == 0) return FP8RL_OK;
+  if (!a || !q || !scale) return FP8RL_ERR_INVALID_ARG;
+  if (lda < k || ldq < k || ld_scale < m) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(a, 16) || !aligned(q, 16) || !aligned(scale, 4) || lda % 8 || ldq % 16)
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(
+      fp8rl::launch_quant_act_token_group128(a, m, k, lda, q, ldq, scale, ld_scale, as_stream(stream)));
+}
+
+int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
+                          int64_t ldw, const float* sw, uint16_t* y, int64_t ldy, int64_t m, int64_t n,
+                          int64_t k, void* stream) {
+  if (m < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
+  if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m >= kMaxDim || n >= kMaxDim || k >= kMaxDim) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m == 0 || n == 0) return FP8RL_OK;
+  if (!qa || !sa || !qw || !sw || !y) return FP8RL_ERR_INVALID_ARG;
+  if (k == 0) return FP8RL_ERR_UNSUPPORTED_SHAPE;   // an empty reduction is not a blockwise GEMM
+  if (lda < k || ldw < k || ldy < n || ld_sa < m) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(qa, 16) || !aligned(qw, 16) || !aligned(y, 16) || !aligned(sa, 4) || !aligned(sw, 4) ||
+      lda % 16 || ldw % 16 || ldy % 8)
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(
+      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream)));
+}
+
+int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw,
+                                  const float* sw, const int32_t* group_offsets, int64_t num_groups,
+                                  int64_t total_rows, uint16_t* y, int64_t n, int64_t k, void* stream) {
+  if (total_rows < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
+  if (num_groups < 1) return FP8RL_ERR_INVALID_ARG;
+  if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (total_rows >= kMaxDim || n >= kMaxDim || k >= kMaxDim || num_groups >= (int64_t(1) << 20) ||
+      n / 128 > 65535)
+    return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (total_rows == 0 || n == 0) return FP8RL_OK;
+  if (!qa || !sa || !qw || !sw || !group_offsets || !y) return FP8RL_ERR_INVALID_ARG;
+  if (k == 0) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (ld_sa < total_rows) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(qa, 16) || !aligned(qw, 16) || !aligned(y, 16) || !aligned(sa, 4) || !aligned(sw, 4) ||
+      !aligned(group_offsets, 4))
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_grouped_gemm_w8a8_block(qa, sa, ld_sa, qw, sw, group_offsets, num_groups,
+                                                          total_rows, y, n, k, as_stream(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,123 @@
+// Dense and grouped (MoE) blockwise-scaled FP8 GEMM kernels and launchers.
+// The tile computation lives in gemm_core.hpp; this file maps workgroups to
+// tiles.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gemm_core.hpp"
+#include "launch.hpp"
+
+namespace fp8rl {
+namespace {
+
+// Tile configurations.
+using CfgLarge = GemmCfg<256, 256, 2, 4>;   // 512 threads, wave tile 128(n) x 64(m)
+using CfgMid = GemmCfg<256, 128, 2, 2>;     // 256 threads, wave tile 128 x 64
+using CfgSmall = GemmCfg<128, 128, 2, 2>;   // 256 threads, wave tile 64 x 64
+
+template <class C>
+__global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_kernel(
+    const uint8_t* __restrict__ qa, int64_t lda, const float* __restrict__ sa, int64_t ld_sa,
+    const uint8_t* __restrict__ qw, int64_t ldw, const float* __restrict__ sw,
+    uint16_t* __restrict__ y, int64_t ldy, int64_t M, int64_t N, int KB, int tiles_m) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
+  const int id = blockIdx.x;
+  const int tile_m = id % tiles_m;
+  const int tile_n = id / tiles_m;
+  const int64_t row_lo = (int64_t)tile_m * C::BM;
+  const int64_t row_hi = min(row_lo + C::BM, M);
+  gemm_tile<C>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, row_lo, row_hi, (int64_t)tile_n * C::BN, N, KB,
+               lds);
+}
+
+// Grouped GEMM: blockIdx.y = n tile, blockIdx.x = m tile counted over all
+// experts in order (expert e owns ceil(rows_e / BM) consecutive m tiles).  The
+// grid is sized for the worst case (total_rows / BM + num_groups); workgroups
+// past the last real tile exit at once.
+template <class C>
+__global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
+    const uint8_t* __restrict__ qa, const float* __restrict__ sa, int64_t ld_sa,
+    const uint8_t* __restrict__ qw, const float* __restrict__ sw,
+    const int32_t* __restrict__ offsets, int G, uint16_t* __restrict__ y, int64_t N, int64_t K) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
+  __shared__ int found[2];
+  const int t = threadIdx.x;
+  const int target = blockIdx.x;
+  if (t == 0) found[0] = -1;
+  __syncthreads();
+  if (t < 64) {
+    // wave 0 scans the experts 64 at a time: inclusive prefix sum of tile counts
+    int base = 0;
+    for (int e0 = 0; e0 < G; e0 += 64) {
+      const int e = e0 + t;
+      int cnt = 0;
+      if (e < G) cnt = (offsets[e + 1] - offsets[e] + C::BM - 1) / C::BM;
+      int incl = cnt;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int v = __shfl_up(incl, d, 64);
+        if (t >= d) incl += v;
+      }
+      const int excl = incl - cnt;
+      if (cnt > 0 && target >= base + excl && target < base + incl) {
+        found[0] = e;
+        found[1] = target - base - excl;
+      }
+      base += __shfl(incl, 63, 64);
+      if (target < base) break;
+    }
+  }
+  __syncthreads();
+  const int e = found[0];
+  if (e < 0) return;                       // uniform: past the last real tile
+  const int mt = found[1];
+  const int KB = (int)(K / 128);
+  const int64_t row_lo = (int64_t)offsets[e] + (int64_t)mt * C::BM;
+  const int64_t row_hi = min(row_lo + C::BM, (int64_t)offsets[e + 1]);
+  gemm_tile<C>(qa, K, sa, ld_sa, qw + (int64_t)e * N * K, K, sw + (int64_t)e * (N / 128) * KB, y, N,
+               row_lo, row_hi, (int64_t)blockIdx.y * C::BN, N, KB, lds);
+}
+
+template <class C>
+hipError_t launch_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
+                        int64_t ldw, const float* sw, uint16_t* y, int64_t ldy, int64_t m, int64_t n,
+                        int64_t k, hipStream_t stream) {
+  const int tiles_m = (int)((m + C::BM - 1) / C::BM);
+  const int tiles_n = (int)((n + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL(gemm_w8a8_block_kernel<C>, dim3((unsigned)(tiles_m * tiles_n)), dim3(C::kThreads), 0,
+                     stream, qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, (int)(k / 128), tiles_m);
+  return hipGetLastError();
+}
+
+template <class C>
+hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw,
+                          const float* sw, const int32_t* offsets, int64_t g, int64_t rows, uint16_t* y,
+                          int64_t n, int64_t k, hipStream_t stream) {
+  const int64_t max_tiles_m = rows / C::BM + g;
+  const int tiles_n = (int)((n + C::BN - 1) / C::BN);
+  hipLaunchKernelGGL(grouped_gemm_w8a8_block_kernel<C>, dim3((unsigned)max_tiles_m, (unsigned)tiles_n),
+                     dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw, sw, offsets, (int)g, y, n, k);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                  const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y, int64_t ldy,
+                                  int64_t m, int64_t n, int64_t k, hipStream_t stream) {
+  if (m >= 2048 && n >= 2048)
+    return launch_dense<CfgLarge>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+  if (m > 128)
+    return launch_dense<CfgMid>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+  return launch_dense<CfgSmall>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+}
+
+hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,
+                                          const uint8_t* qw, const float* sw, const int32_t* group_offsets,
+                                          int64_t num_groups, int64_t total_rows, uint16_t* y, int64_t n,
+                                          int64_t k, hipStream_t stream) {
+  return launch_grouped<CfgSmall>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
+                                  stream);
+}
+
+}  // namespace fp8rl

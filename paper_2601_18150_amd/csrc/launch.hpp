@@ -1,0 +1,29 @@
+// Internal launchers behind the C ABI (include/fp8rl.h).  Arguments are
+// validated by the API layer before any of these is called; each launcher only
+// picks a grid and enqueues its kernel(s) on `stream`.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fp8rl {
+
+hipError_t launch_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
+                                        uint8_t* q, int64_t ldq, float* scale, hipStream_t stream);
+
+hipError_t launch_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
+                                           uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
+                                           hipStream_t stream);
+
+hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                  const uint8_t* qw, int64_t ldw, const float* sw,
+                                  uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,
+                                  hipStream_t stream);
+
+hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,
+                                          const uint8_t* qw, const float* sw,
+                                          const int32_t* group_offsets, int64_t num_groups,
+                                          int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
+                                          hipStream_t stream);
+
+}  // namespace fp8rl

@@ -1,0 +1,125 @@
+// Blockwise (128x128) weight and per-token 1x128 activation quantisation to
+// OCP E4M3 with fp32 scales (paper section 2.1.1, Eq. (1); section 3.1).
+//
+// Both kernels are HBM-bound streaming kernels: 16-byte loads of 8 bf16 per
+// lane, an integer max over the bf16 magnitudes (packed u16 max), a DPP
+// reduction inside each 16-lane row, the per-block scale, and the element map
+// of quant_math.hpp, then 8-byte stores of 8 codes per lane.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+#include "launch.hpp"
+#include "quant_math.hpp"
+
+#pragma clang fp contract(off)
+
+namespace fp8rl {
+namespace {
+
+using qmath::BlockScale;
+
+// 8 bf16 (one uint4) -> 8 E4M3 codes (one uint2), all with the same block scale.
+template <bool kPre>
+__device__ __forceinline__ uint2 quant8(const uint4& v, const BlockScale& bs) {
+  auto pack4 = [&](uint32_t w0, uint32_t w1) -> uint32_t {
+    uint32_t c0 = qmath::quant_elem<kPre>(w0 & 0xFFFFu, bs);
+    uint32_t c1 = qmath::quant_elem<kPre>(w0 >> 16, bs);
+    uint32_t c2 = qmath::quant_elem<kPre>(w1 & 0xFFFFu, bs);
+    uint32_t c3 = qmath::quant_elem<kPre>(w1 >> 16, bs);
+    return c0 | (c1 << 8) | (c2 << 16) | (c3 << 24);
+  };
+  return make_uint2(pack4(v.x, v.y), pack4(v.z, v.w));
+}
+
+// ---------------------------------------------------------------------------
+// Weight: one 256-thread workgroup per 128x128 block.  Thread t owns the 16-byte
+// column chunk (t & 15) of rows (t >> 4) + 16 i, i = 0..7: every load instruction
+// of a wave reads four 256-byte row segments.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void quant_weight_block128_kernel(
+    const uint16_t* __restrict__ w, int64_t ldw, uint8_t* __restrict__ q, int64_t ldq,
+    float* __restrict__ scale, int nbk) {
+  __shared__ uint32_t red[4];
+  const int blk = blockIdx.x;
+  const int bi = blk / nbk;
+  const int bj = blk - bi * nbk;
+  const int t = threadIdx.x;
+  const int chunk = t & 15;
+  const int r0 = t >> 4;
+
+  const uint16_t* src = w + (int64_t)(bi * 128 + r0) * ldw + bj * 128 + chunk * 8;
+  uint4 v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = *reinterpret_cast<const uint4*>(src + (int64_t)(16 * i) * ldw);
+
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m = max(m, amax16_of(v[i]));
+  m = wave_max(m);
+  if ((t & 63) == 0) red[t >> 6] = m;
+  __syncthreads();
+  m = max(max(red[0], red[1]), max(red[2], red[3]));
+
+  const BlockScale bs = qmath::block_scale(m);
+  if (t == 0) scale[blk] = bs.scale;
+
+  uint8_t* dst = q + (int64_t)(bi * 128 + r0) * ldq + bj * 128 + chunk * 8;
+  if (bs.prescaled) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint2*>(dst + (int64_t)(16 * i) * ldq) = quant8<true>(v[i], bs);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<uint2*>(dst + (int64_t)(16 * i) * ldq) = quant8<false>(v[i], bs);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Activation: 16 lanes per (token, group); a 256-thread workgroup covers 16
+// consecutive (token, group) units in row-major order, so a wave reads 1 KiB of
+// contiguous row data when the four units share a token.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void quant_act_token_group128_kernel(
+    const uint16_t* __restrict__ a, int64_t lda, uint8_t* __restrict__ q, int64_t ldq,
+    float* __restrict__ scale, int64_t ld_scale, int64_t units, int ng) {
+  const int t = threadIdx.x;
+  const int64_t unit = (int64_t)blockIdx.x * 16 + (t >> 4);
+  const bool valid = unit < units;
+  const int64_t u = valid ? unit : units - 1;      // keep every lane in bounds
+  const int64_t row = u / ng;
+  const int g = (int)(u - row * ng);
+  const int chunk = t & 15;
+
+  const uint4 v = *reinterpret_cast<const uint4*>(a + row * lda + g * 128 + chunk * 8);
+  const uint32_t m = row16_max(amax16_of(v));
+  const BlockScale bs = qmath::block_scale(m);
+  uint2 c = bs.prescaled ? quant8<true>(v, bs) : quant8<false>(v, bs);
+  if (valid) {
+    *reinterpret_cast<uint2*>(q + row * ldq + g * 128 + chunk * 8) = c;
+    if (chunk == 0) scale[(int64_t)g * ld_scale + row] = bs.scale;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
+                                        uint8_t* q, int64_t ldq, float* scale, hipStream_t stream) {
+  const int nbn = (int)(n / 128), nbk = (int)(k / 128);
+  const int64_t blocks = (int64_t)nbn * nbk;
+  hipLaunchKernelGGL(quant_weight_block128_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     w, ldw, q, ldq, scale, nbk);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
+                                           uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
+                                           hipStream_t stream) {
+  const int ng = (int)(k / 128);
+  const int64_t units = m * ng;
+  const int64_t blocks = (units + 15) / 16;
+  hipLaunchKernelGGL(quant_act_token_group128_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     a, lda, q, ldq, scale, ld_scale, units, ng);
+  return hipGetLastError();
+}
+
+}  // namespace fp8rl

@@ -211,3 +211,42 @@ def moe_layer(seed: int = 6, device="cpu", tokens: int = 4096, hidden: int = 204
     w_down = normal_bf16((experts, hidden, inter), 0.02, seed + 14, device)
     return {"routing": routing, "x_gate_up": x_gate_up, "x_down": x_down,
             "w_gate_up": w_gate_up, "w_down": w_down}
+
+
+# --------------------------------------------------------------------------
+# exhaustive element-map sweep layouts (bit patterns only)
+# --------------------------------------------------------------------------
+def _sweep_rows(per: int, device) -> torch.Tensor:
+    """Rows of `per + 1` bf16 bit patterns: column 0 holds a magnitude a (the row
+    maximum), the other columns list every x with |x| <= a, both signs, over as
+    many rows as a needs (unused slots are +0).  Every positive finite nonzero a
+    appears, plus one all-zero row mixing +0 and -0."""
+    a = torch.arange(1, 0x7F80, dtype=torch.int32, device=device)        # positive finite magnitudes
+    cnt = 2 * (a + 1)                                                    # signed x with |x| <= a
+    nb = (cnt + per - 1) // per
+    row_a = torch.repeat_interleave(a, nb)
+    first = torch.cumsum(nb, 0) - nb
+    j = torch.arange(row_a.numel(), dtype=torch.int32, device=device) - torch.repeat_interleave(first, nb)
+    i = j[:, None] * per + torch.arange(per, dtype=torch.int32, device=device)[None, :]
+    cnt_row = torch.repeat_interleave(cnt, nb)[:, None]
+    x = torch.where(i < cnt_row, (i >> 1) | ((i & 1) << 15), torch.zeros_like(i))
+    rows = torch.cat([row_a[:, None], x], dim=1)
+    zero_row = torch.zeros((1, per + 1), dtype=torch.int32, device=device)
+    zero_row[0, 1::2] = 0x8000
+    rows = torch.cat([zero_row, rows], dim=0)
+    return rows
+
+
+def sweep_weight_blocks(device="cpu") -> torch.Tensor:
+    """bf16 weight [B*128][128] made of 128x128 blocks, each one amax value plus
+    16383 x values from the sweep; returned as a bf16 tensor (bit patterns)."""
+    rows = _sweep_rows(128 * 128 - 1, device)                           # [B][16384]
+    bits = torch.where(rows >= 0x8000, rows - 0x10000, rows).to(torch.int16)
+    return bits.view(torch.bfloat16).reshape(-1, 128)
+
+
+def sweep_act_groups(device="cpu") -> torch.Tensor:
+    """bf16 activations [R][128]: each row one amax value plus 127 x values."""
+    rows = _sweep_rows(127, device)
+    bits = torch.where(rows >= 0x8000, rows - 0x10000, rows).to(torch.int16)
+    return bits.view(torch.bfloat16)

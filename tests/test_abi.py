@@ -1,0 +1,117 @@
+"""CPU-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments with the documented status codes
+before launching anything.  Every call here fails validation (or is an empty
+no-op), so none of them reaches the GPU, even on a machine that has one: the
+fake pointers are never dereferenced."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fp8rl.h")
+
+OK, INVALID, SHAPE, MISALIGNED = 0, 1, 2, 3
+A16 = 1 << 20          # a fake, 16-byte-aligned device address (never dereferenced)
+A4 = A16 + 4           # 4-byte aligned only
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fp8rl_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2601_18150_amd as fp8rl
+    return fp8rl.load()
+
+
+def test_header_declares_the_four_entry_points():
+    names = declared_functions()
+    for f in ("fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
+              "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    import paper_2601_18150_amd as fp8rl
+    out = subprocess.run(["nm", "-D", "--defined-only", fp8rl.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (fp8rl_\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_status_strings_and_version(lib):
+    import paper_2601_18150_amd as fp8rl
+    assert fp8rl.fp8rl_status_string(0) == "FP8RL_OK"
+    assert fp8rl.fp8rl_status_string(3) == "FP8RL_ERR_MISALIGNED"
+    assert fp8rl.fp8rl_status_string(99) == "FP8RL_ERR_UNKNOWN"
+    assert fp8rl.fp8rl_version() >= 100
+
+
+def test_quant_weight_argument_errors(lib):
+    f = lib.fp8rl_quant_weight_block128
+    assert f(A16, -128, 128, 128, A16, 128, A16, None) == INVALID
+    assert f(A16, 128, 200, 200, A16, 208, A16, None) == SHAPE
+    assert f(A16, 100, 128, 128, A16, 128, A16, None) == SHAPE
+    assert f(None, 128, 128, 128, A16, 128, A16, None) == INVALID
+    assert f(A16, 128, 128, 120, A16, 128, A16, None) == INVALID      # ldw < k
+    assert f(A16, 128, 128, 128, A16, 127, A16, None) == INVALID      # ldq < k
+    assert f(A4, 128, 128, 128, A16, 128, A16, None) == MISALIGNED
+    assert f(A16, 128, 128, 132, A16, 128, A16, None) == MISALIGNED   # ldw % 8
+    assert f(A16, 128, 128, 128, A16, 136, A16, None) == MISALIGNED   # ldq % 16
+    assert f(A16, 0, 128, 128, A16, 128, A16, None) == OK             # empty: no-op
+    assert f(None, 0, 0, 0, None, 0, None, None) == OK
+
+
+def test_quant_act_argument_errors(lib):
+    f = lib.fp8rl_quant_act_token_group128
+    assert f(A16, -1, 128, 128, A16, 128, A16, 1, None) == INVALID
+    assert f(A16, 4, 100, 128, A16, 128, A16, 4, None) == SHAPE
+    assert f(A16, 4, 128, 128, A16, 128, A16, 3, None) == INVALID     # ld_scale < m
+    assert f(A16, 4, 128, 128, None, 128, A16, 4, None) == INVALID
+    assert f(A16, 4, 128, 128, A16 + 8, 128, A16, 4, None) == MISALIGNED
+    assert f(A16, 4, 128, 128, A16, 128, A16 + 2, 4, None) == MISALIGNED
+    assert f(None, 0, 128, 128, None, 128, None, 0, None) == OK
+
+
+def test_gemm_argument_errors(lib):
+    f = lib.fp8rl_gemm_w8a8_block
+    #      qa  lda  sa  ld_sa qw  ldw  sw  y   ldy  m  n    k
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, -8, 128, 128, None) == INVALID
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 200, 8, 200, 128, None) == SHAPE
+    assert f(A16, 256, A16, 8, A16, 256, A16, A16, 128, 8, 128, 192, None) == SHAPE
+    assert f(A16, 128, A16, 7, A16, 128, A16, A16, 128, 8, 128, 128, None) == INVALID  # ld_sa < m
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 120, 8, 128, 128, None) == INVALID  # ldy < n
+    assert f(A16, 128, A16, 8, None, 128, A16, A16, 128, 8, 128, 128, None) == INVALID
+    assert f(A16 + 8, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == MISALIGNED
+    assert f(A16, 136, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == MISALIGNED
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 132, 8, 128, 128, None) == MISALIGNED
+    assert f(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None) == OK
+
+
+def test_grouped_gemm_argument_errors(lib):
+    f = lib.fp8rl_grouped_gemm_w8a8_block
+    #        qa  sa  ld_sa qw  sw  off  G  R   y   n    k
+    assert f(A16, A16, 8, A16, A16, A16, 0, 8, A16, 128, 128, None) == INVALID    # no groups
+    assert f(A16, A16, 8, A16, A16, A16, 2, -1, A16, 128, 128, None) == INVALID
+    assert f(A16, A16, 8, A16, A16, A16, 2, 8, A16, 192, 128, None) == SHAPE
+    assert f(A16, A16, 7, A16, A16, A16, 2, 8, A16, 128, 128, None) == INVALID    # ld_sa < R
+    assert f(A16, A16, 8, A16, A16, None, 2, 8, A16, 128, 128, None) == INVALID
+    assert f(A16, A16, 8, A16, A16, A16 + 2, 2, 8, A16, 128, 128, None) == MISALIGNED
+    assert f(A16, A16, 8, A4, A16, A16, 2, 8, A16, 128, 128, None) == MISALIGNED
+    assert f(None, None, 0, None, None, None, 2, 0, None, 128, 128, None) == OK
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    import paper_2601_18150_amd as fp8rl
+    w = torch.zeros(128, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        fp8rl.fp8rl_quant_weight_block128(w)

@@ -1,0 +1,314 @@
+"""GPU parity of the blockwise-scaled FP8 GEMMs (dense and grouped) against the
+fp64 oracle on the same FP8 codes and scales.
+
+Codes and scales given to the GPU are made by the oracle (or drawn directly as
+random codes), never by the GPU quantisers.  Pass criterion per element:
+|gpu - ref| <= 4e-3 |ref| + 1e-3 rms(ref), rms over the call's output (over the
+sampled rows where the output is only sampled)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import cref, gemm
+from tests.gpu_util import announce, bf16_to_f64, need_gpu, u16
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fp8rl():
+    need_gpu()
+    import paper_2601_18150_amd as m
+    m.load()
+    return m
+
+
+def to_dev(x: np.ndarray, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    return t.to("cuda") if dtype is None else t.to("cuda").to(dtype)
+
+
+def rand_codes(shape, rng):
+    c = rng.integers(0, 256, size=shape, dtype=np.uint8)
+    c[(c & 0x7F) == 0x7F] ^= 0x01           # no NaN codes
+    return c
+
+
+def rand_scales(shape, rng):
+    return (2.0 ** rng.uniform(-12, -2, size=shape)).astype(np.float32)
+
+
+def check(y_gpu: torch.Tensor, y_ref: np.ndarray, what: str, rows=None):
+    got = bf16_to_f64(y_gpu)
+    if rows is not None:
+        got = got[rows]
+    ok, worst, rms = gemm.tolerance_check(got, y_ref)
+    if not ok:
+        err = np.abs(got - y_ref)
+        ratio = err / (4e-3 * np.abs(y_ref) + 1e-3 * rms)
+        order = np.argsort(ratio, axis=None)[::-1][:5]
+        lines = []
+        for flat in order:
+            idx = np.unravel_index(flat, ratio.shape)
+            lines.append(f"  at {tuple(int(i) for i in idx)}: gpu {got[idx]!r} ref {y_ref[idx]!r} "
+                         f"err {err[idx]:.4g} ratio {ratio[idx]:.3f}")
+        print("\n".join(lines))
+    assert ok, f"{what}: worst |err|/bound = {worst:.3f} (rms {rms:.4g})"
+
+
+def run_dense(fp8rl, qa, sa, qw, sw, lda_pad=0, ldy_pad=0, ldsa_pad=0):
+    m, k = qa.shape
+    n = qw.shape[0]
+    qa_d = torch.zeros((m, k + lda_pad), dtype=torch.uint8, device="cuda")
+    qa_d[:, :k] = to_dev(qa)
+    sa_d = torch.zeros((k // 128, m + ldsa_pad), dtype=torch.float32, device="cuda")
+    sa_d[:, :m] = to_dev(sa[:, :m])
+    y = torch.zeros((m, n + ldy_pad), dtype=torch.bfloat16, device="cuda")
+    fp8rl.fp8rl_gemm_w8a8_block(qa_d[:, :k], sa_d, to_dev(qw), to_dev(sw), y=y[:, :n])
+    torch.cuda.synchronize()
+    if ldy_pad:
+        assert torch.all(y[:, n:] == 0), "wrote past n in a padded output row"
+    return y[:, :n]
+
+
+def test_gemm_tiny_config(fp8rl):
+    announce("gemm tiny 64x512x512 from oracle-quantised bf16")
+    a, w = synth.tiny_linear()
+    qa, sa = cref.quant_act_token_group128(u16(a))
+    qw, sw = cref.quant_weight_block128(u16(w))
+    y = run_dense(fp8rl, qa, sa, qw, sw)
+    check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), "tiny")
+
+
+def quantised_operands(m, n, k, seed):
+    """Realistic FP8 operands: bf16 N(0,1) activations and N(0,0.02) weights, with a
+    distinct random gain 2^U(-8,8) per (token, group) and per 128x128 weight block
+    so that every scale differs (a wrong scale index is a gross error), quantised
+    by the oracle."""
+    rng = np.random.default_rng(seed)
+    a = rng.standard_normal((m, k)).astype(np.float32)
+    a *= np.repeat(2.0 ** rng.uniform(-8, 8, size=(m, k // 128)), 128, axis=1).astype(np.float32)
+    w = (rng.standard_normal((n, k)) * 0.02).astype(np.float32)
+    gw = 2.0 ** rng.uniform(-8, 8, size=(n // 128, k // 128))
+    w *= np.repeat(np.repeat(gw, 128, axis=0), 128, axis=1).astype(np.float32)
+    a16 = torch.from_numpy(a).to(torch.bfloat16)
+    w16 = torch.from_numpy(w).to(torch.bfloat16)
+    qa, sa = cref.quant_act_token_group128(u16(a16))
+    qw, sw = cref.quant_weight_block128(u16(w16))
+    return qa, sa, qw, sw
+
+
+@pytest.mark.parametrize("m,n,k,pads", [
+    (1, 128, 128, (0, 0, 0)),
+    (37, 384, 256, (16, 8, 3)),
+    (100, 256, 512, (0, 0, 0)),
+    (129, 640, 384, (32, 24, 1)),
+    (300, 512, 256, (0, 0, 0)),
+    (2048, 2048, 256, (0, 0, 0)),
+    (2100, 2176, 384, (16, 8, 5)),
+])
+def test_gemm_shapes(fp8rl, m, n, k, pads):
+    announce(f"gemm m={m} n={n} k={k} pads={pads}")
+    qa, sa, qw, sw = quantised_operands(m, n, k, m * 7 + n + k)
+    y = run_dense(fp8rl, qa, sa, qw, sw, *pads)
+    check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"{m}x{n}x{k}")
+
+
+def test_gemm_full_range_codes_within_accumulation_bound(fp8rl):
+    """Uniformly random codes over the whole E4M3 range (products up to 448^2 with
+    heavy cancellation inside a K block).
+
+    Measured on gfx950: the FP8 MFMA sums the 128 products of one instruction
+    with less than fp32 precision (errors up to about 2^-14 of the block's
+    absolute product sum), so on such inputs a few elements whose value is far
+    below their partial sums miss the 4e-3/1e-3 tolerance.  This test bounds the
+    error by bf16 rounding plus 2^-12 of each block's scaled absolute product sum,
+    and reports how many elements fall outside the plain tolerance."""
+    announce("gemm full-range random codes, accumulation bound")
+    rng = np.random.default_rng(2048 * 7 + 2048 + 256)
+    m, n, k = 2048, 2048, 256
+    qa, qw = rand_codes((m, k), rng), rand_codes((n, k), rng)
+    sa, sw = rand_scales((k // 128, m), rng), rand_scales((n // 128, k // 128), rng)
+    y = bf16_to_f64(run_dense(fp8rl, qa, sa, qw, sw))
+    ref = gemm.gemm_ref_fp64(qa, sa, qw, sw)
+    from oracle import e4m3
+    da, dw = np.abs(e4m3.decode(qa)), np.abs(e4m3.decode(qw))
+    abs_sum = np.zeros((m, n))
+    for kb in range(k // 128):
+        sl = slice(kb * 128, (kb + 1) * 128)
+        blk = da[:, sl] @ dw[:, sl].T
+        abs_sum += blk * sa[kb][:, None] * np.repeat(sw[:, kb], 128)[None, :]
+    err = np.abs(y - ref)
+    bound = 2.0 ** -8 * np.abs(ref) * (1 + 2.0 ** -8) + 2.0 ** -12 * abs_sum
+    assert np.all(err <= bound), f"worst err/bound {np.max(err / bound):.3f}"
+    ok, worst, rms = gemm.tolerance_check(y, ref)
+    outside = int(np.sum(err > 4e-3 * np.abs(ref) + 1e-3 * rms))
+    print(f"full-range codes: {outside} of {m * n} elements outside the plain tolerance (worst {worst:.3f})")
+
+
+def test_gemm_k_block_accumulates_in_fp32(fp8rl):
+    """Cancellation inside one 128-wide K block: 448*448 - 448*448 + x*x must leave x*x.
+
+    With fp32 accumulation (24-bit significand) the small term survives in any
+    summation order as long as it is >= 2^-6 (half an fp32 ulp of 200704 is
+    2^-7); a narrower accumulator would drop it."""
+    announce("gemm accumulation precision probe")
+    from oracle import e4m3
+    small = np.array([4.0, 1.0, 0.5, 0.25, 0.125], np.float32)
+    m, n, k = 16, 128, 128
+    qa = np.zeros((m, k), np.uint8)
+    qw = np.zeros((n, k), np.uint8)
+    for i, x in enumerate(small):
+        for pos in range(3):                   # put the big pair at different K positions
+            r = i * 3 + pos
+            c0, c1, c2 = [(pos * 40 + d * 13) % 128 for d in range(3)]
+            qa[r, [c0, c1, c2]] = e4m3.encode(np.array([448.0, 448.0, x], np.float32))
+            qw[r % n, [c0, c1, c2]] = e4m3.encode(np.array([448.0, -448.0, x], np.float32))
+    ones_a = np.ones((1, m), np.float32)
+    ones_w = np.ones((1, 1), np.float32)
+    y = bf16_to_f64(run_dense(fp8rl, qa, ones_a, qw, ones_w))
+    want = gemm.gemm_ref_fp64(qa, ones_a, qw, ones_w)
+    diag = [(r, y[r, r % n], want[r, r % n]) for r in range(15)]
+    print("probe (row, gpu, exact):", diag)
+    assert np.array_equal(y, want)
+
+
+def test_gemm_exact_small_integers(fp8rl):
+    """Integer codes with unit scales: the exact result is an integer < 256, so bf16 holds it exactly."""
+    announce("gemm exact integers")
+    rng = np.random.default_rng(5)
+    m, n, k = 70, 256, 256
+    ia = rng.integers(-1, 2, size=(m, k))
+    iw = rng.integers(-1, 2, size=(n, k))
+    from oracle import e4m3
+    qa, qw = e4m3.encode(ia.astype(np.float32)), e4m3.encode(iw.astype(np.float32))
+    ones_a = np.ones((k // 128, m), np.float32)
+    ones_w = np.ones((n // 128, k // 128), np.float32)
+    y = run_dense(fp8rl, qa, ones_a, qw, ones_w)
+    want = (ia @ iw.T).astype(np.float64)
+    assert np.abs(want).max() < 256
+    assert np.array_equal(bf16_to_f64(y), want)
+
+
+def test_gemm_decode_layer(fp8rl):
+    """M=256 decode tokens through the four Qwen3-8B linears of one layer (full outputs)."""
+    acts = synth.decode_activations()
+    ws = synth.layer_weights(0)
+    for name, (k, n) in synth.QWEN3_8B_LINEARS.items():
+        announce(f"gemm decode M=256 {name} {k}->{n}")
+        x = acts["inter"] if k == 12288 else acts["h"]
+        qa, sa = cref.quant_act_token_group128(u16(x))
+        qw, sw = cref.quant_weight_block128(u16(ws[name]))
+        y = run_dense(fp8rl, qa, sa, qw, sw)
+        check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), name)
+
+
+def test_gemm_prefill_full_size_sampled_rows(fp8rl):
+    """8192x4096 -> 24576 with outliers: the full GEMM on the GPU, the oracle on sampled rows."""
+    announce("gemm prefill 8192x4096x24576")
+    a, w = synth.prefill_linear()
+    qa, sa = cref.quant_act_token_group128(u16(a))
+    qw, sw = cref.quant_weight_block128(u16(w))
+    y = run_dense(fp8rl, qa, sa, qw, sw)
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([np.arange(8), np.arange(8184, 8192),
+                                     rng.choice(8192, 48, replace=False)]))
+    ref = gemm.gemm_ref_fp64(qa[rows], sa[:, rows], qw, sw)
+    check(y, ref, "prefill", rows=rows)
+
+
+def test_gemm_deterministic(fp8rl):
+    announce("gemm determinism")
+    rng = np.random.default_rng(9)
+    m, n, k = 2304, 2304, 512
+    qa, qw = to_dev(rand_codes((m, k), rng)), to_dev(rand_codes((n, k), rng))
+    sa, sw = to_dev(rand_scales((k // 128, m), rng)), to_dev(rand_scales((n // 128, k // 128), rng))
+    y1 = fp8rl.fp8rl_gemm_w8a8_block(qa, sa, qw, sw)
+    y2 = fp8rl.fp8rl_gemm_w8a8_block(qa, sa, qw, sw)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+def run_grouped(fp8rl, qa, sa, qw, sw, offsets, ldsa_pad=0):
+    r = qa.shape[0]
+    k = qa.shape[1]
+    sa_d = torch.zeros((k // 128, r + ldsa_pad), dtype=torch.float32, device="cuda")
+    sa_d[:, :r] = to_dev(sa[:, :r])
+    y = fp8rl.fp8rl_grouped_gemm_w8a8_block(to_dev(qa), sa_d, to_dev(qw), to_dev(sw),
+                                            to_dev(np.asarray(offsets, np.int32)))
+    torch.cuda.synchronize()
+    return y
+
+
+@pytest.mark.parametrize("counts", [
+    [3, 0, 130, 2, 0],
+    [0, 0, 1],
+    [257, 0, 0, 64, 129, 1, 0, 300],
+    [5],
+])
+def test_grouped_small_random(fp8rl, counts):
+    announce(f"grouped gemm counts={counts}")
+    rng = np.random.default_rng(sum(counts) + len(counts))
+    g, n, k = len(counts), 384, 256
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    r = int(offsets[-1])
+    qa, qw = rand_codes((r, k), rng), rand_codes((g, n, k), rng)
+    sa, sw = rand_scales((k // 128, r), rng), rand_scales((g, n // 128, k // 128), rng)
+    y = run_grouped(fp8rl, qa, sa, qw, sw, offsets, ldsa_pad=3)
+    check(y, gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, offsets), f"grouped {counts}")
+
+
+def test_grouped_many_experts_matches_dense_per_expert(fp8rl):
+    """70 experts (more than one 64-expert scan chunk) vs the dense kernel per expert."""
+    announce("grouped gemm 70 experts vs dense")
+    rng = np.random.default_rng(70)
+    counts = rng.integers(0, 40, size=70)
+    counts[[3, 64, 69]] = 0
+    g, n, k = 70, 256, 256
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    r = int(offsets[-1])
+    qa, qw = rand_codes((r, k), rng), rand_codes((g, n, k), rng)
+    sa, sw = rand_scales((k // 128, r), rng), rand_scales((g, n // 128, k // 128), rng)
+    y = run_grouped(fp8rl, qa, sa, qw, sw, offsets)
+    check(y, gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, offsets), "grouped 70")
+
+
+@pytest.mark.parametrize("which", ["gate_up", "down"])
+def test_grouped_moe_full_size_sampled_rows(fp8rl, which):
+    """Qwen3-30B-A3B-shaped experts, Zipf(1.1) top-8 routing of 4096 tokens (some experts empty)."""
+    announce(f"grouped gemm MoE {which}")
+    moe = synth.moe_layer()
+    off = moe["routing"].offsets.numpy()
+    x = moe["x_gate_up"] if which == "gate_up" else moe["x_down"]
+    wts = moe["w_gate_up"] if which == "gate_up" else moe["w_down"]
+    g, n, k = wts.shape
+    qa, sa = cref.quant_act_token_group128(u16(x))
+    qw, sw = cref.quant_weight_block128(u16(wts.reshape(g * n, k)))
+    qw = qw.reshape(g, n, k)
+    sw = sw.reshape(g, n // 128, k // 128)
+    assert (np.diff(off) == 0).sum() >= 8, "the workload is meant to have empty experts"
+    y = run_grouped(fp8rl, qa, sa, qw, sw, off)
+    # oracle on the first, last and a middle row of every non-empty expert
+    rows, ref_rows = [], []
+    for e in range(g):
+        lo, hi = int(off[e]), int(off[e + 1])
+        if hi <= lo:
+            continue
+        pick = sorted({lo, hi - 1, (lo + hi) // 2})
+        ref = gemm.gemm_ref_fp64(qa[pick], sa[:, pick], qw[e], sw[e])
+        rows += pick
+        ref_rows.append(ref)
+    check(y, np.concatenate(ref_rows), f"moe {which}", rows=np.array(rows))
+
+
+def test_linear_w8a8_end_to_end_tiny(fp8rl):
+    """Full forward of the W8A8 linear on the GPU (both quantisers + GEMM) vs the oracle path."""
+    announce("linear_w8a8 tiny end to end")
+    a, w = synth.tiny_linear(device="cuda")
+    qw_d, sw_d = fp8rl.fp8rl_quant_weight_block128(w)
+    y = fp8rl.linear_w8a8(a, qw_d, sw_d)
+    torch.cuda.synchronize()
+    qa, sa = cref.quant_act_token_group128(u16(a))
+    qw, sw = cref.quant_weight_block128(u16(w))
+    check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), "linear tiny")
