@@ -11,9 +11,9 @@ namespace fp8rl {
 namespace {
 
 // Tile configurations.
-using CfgLarge = GemmCfg<256, 256, 2, 4>;   // 512 threads, wave tile 128(n) x 64(m)
-using CfgMid = GemmCfg<256, 128, 2, 2>;     // 256 threads, wave tile 128 x 64
-using CfgSmall = GemmCfg<128, 128, 2, 2>;   // 256 threads, wave tile 64 x 64
+using CfgLarge = GemmCfg<256, 256, 2, 4, 2>;   // 512 threads, wave tile 128(n) x 64(m), 128 KiB LDS
+using CfgMid = GemmCfg<256, 128, 2, 2, 3>;     // 256 threads, wave tile 128 x 64, 144 KiB LDS
+using CfgSmall = GemmCfg<128, 128, 2, 2, 3>;   // 256 threads, wave tile 64 x 64, 96 KiB LDS
 
 template <class C>
 __global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_kernel(

@@ -14,9 +14,10 @@
 // i.e. the per-K-block scale is applied in the epilogue of each K step.
 //
 // Data movement per K step: the block's W and A tiles (BN x 128 and BM x 128
-// bytes) go global -> registers -> LDS (double-buffered), rows of 128 bytes
-// with the 16-byte chunk index XOR-swizzled by (row & 7) so that the fragment
-// reads (ds_read_b128) of 8 consecutive rows hit 8 distinct bank groups.
+// bytes) go straight from global memory into an LDS ring (global_load_lds,
+// no register staging), rows of 128 bytes with the 16-byte chunk index
+// XOR-swizzled by (row & 7) so that the fragment reads (ds_read_b128) of 8
+// consecutive rows hit 8 distinct bank groups.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -29,12 +30,13 @@ namespace fp8rl {
 typedef int v8i32 __attribute__((ext_vector_type(8)));
 typedef float v4f32 __attribute__((ext_vector_type(4)));
 
-template <int BN_, int BM_, int WN_, int WM_>
+template <int BN_, int BM_, int WN_, int WM_, int STAGES_>
 struct GemmCfg {
   static constexpr int BN = BN_;            // tile extent along n (weight rows)
   static constexpr int BM = BM_;            // tile extent along m (tokens)
   static constexpr int WN = WN_;            // waves along n
   static constexpr int WM = WM_;            // waves along m
+  static constexpr int STAGES = STAGES_;    // LDS ring depth (K steps in flight)
   static constexpr int kWaves = WN * WM;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int WTN = BN / WN;       // wave tile along n
@@ -44,13 +46,15 @@ struct GemmCfg {
   static constexpr int kWBytes = BN * 128;  // one K step of the W tile
   static constexpr int kABytes = BM * 128;
   static constexpr int kStageBytes = kWBytes + kABytes;
-  static constexpr int kLdsBytes = 2 * kStageBytes;
-  static constexpr int kRowStep = kThreads / 8;           // rows covered by one load sweep
-  static constexpr int kWLoads = BN / kRowStep;           // 16-byte loads per thread per K step
-  static constexpr int kALoads = BM / kRowStep;
+  static constexpr int kLdsBytes = STAGES * kStageBytes;
+  // one direct-to-LDS wave instruction moves 8 rows x 128 bytes (1 KiB)
+  static constexpr int kOctets = (BN + BM) / 8;
+  static constexpr int kLoadsPerWave = kOctets / kWaves;
   static_assert(WTN % 16 == 0 && WTM % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(WTN <= 128 && 128 % WTN == 0, "a wave's n range must sit inside one 128-row scale block");
-  static_assert(BN % kRowStep == 0 && BM % kRowStep == 0, "tile rows must be a multiple of the load sweep");
+  static_assert(kOctets % kWaves == 0, "row octets must divide evenly among the waves");
+  static_assert(STAGES >= 2, "need at least double buffering");
+  static_assert(kLdsBytes <= 160 * 1024, "LDS is 160 KiB per CU");
 };
 
 // Byte offset of 16-byte chunk `c` of row `r` in a swizzled 128-byte-row tile.
@@ -73,10 +77,34 @@ __device__ __forceinline__ v4f32 mfma_fp8_16x16x128(const v8i32& a, const v8i32&
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, zero, 0, 0, 0, 0, 0, 0);
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) const void global_void_t;
+
+// 16 bytes per lane, global -> LDS without passing through registers
+// (global_load_lds_dwordx4): lane L of the wave writes LDS bytes
+// [lds_wave_base + 16 L, +16).  lds_wave_base must be wave-uniform.
+__device__ __forceinline__ void lds_dma16(const uint8_t* gptr, uint8_t* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) only (expcnt and lgkmcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
 // One output tile.  Rows row_lo .. row_hi-1 of A / Y are valid for this tile
 // (row_hi - row_lo may be less than BM: loads clamp to the last valid row, stores
 // are masked).  n0 .. n0+BN-1 are the tile's weight rows; rows >= N are clamped
 // on load and masked on store.  sw points at this weight's [N/128][KB] scales.
+//
+// Pipeline (STAGES-deep LDS ring, one barrier per K step):
+//   prologue: DMA K steps 0 .. STAGES-2
+//   step kb:  wait for this wave's DMA of step kb; barrier (all waves' DMA of
+//             step kb landed, all waves done reading step kb-1's slot);
+//             prefetch next step's scales; DMA step kb+STAGES-1 into the slot
+//             freed by step kb-1; MFMA + scale-FMA on slot kb % STAGES.
 template <class C>
 __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_t lda,
                                           const float* __restrict__ sa, int64_t ld_sa,
@@ -93,36 +121,42 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
   const int n_valid = (int)min((int64_t)C::BN, N - n0);        // >= 1
   const int m_valid = (int)(row_hi - row_lo);                  // >= 1
 
-  // ---- global -> LDS copy plan: thread t moves 16-byte chunk (t & 7) of tile
-  //      rows (t >> 3) + i * kRowStep.  Since kRowStep is a multiple of 8,
-  //      (row & 7) and hence the swizzled LDS chunk are fixed per thread.
-  //      Global addresses are a wave-uniform 64-bit base (advanced by 128 bytes
-  //      per K step) plus a 32-bit per-lane offset.
-  const int c8 = t & 7;
-  const int r8 = t >> 3;
-  uint32_t ow[C::kWLoads];
-  uint32_t oa[C::kALoads];
+  // ---- DMA plan: wave w moves row octets w, w + kWaves, ...  In an octet,
+  //      lane L lands at row 8o + (L >> 3), physical chunk (L & 7), which holds
+  //      logical chunk (L & 7) ^ (row & 7) of the swizzled layout.
+  const int lrow = lane >> 3;
+  const int lchunk = (lane & 7) ^ lrow;
+  uint32_t goff[C::kLoadsPerWave];
+  bool is_w[C::kLoadsPerWave];
 #pragma unroll
-  for (int i = 0; i < C::kWLoads; ++i)
-    ow[i] = (uint32_t)(min(r8 + i * C::kRowStep, n_valid - 1) * ldw + c8 * 16);
-#pragma unroll
-  for (int i = 0; i < C::kALoads; ++i)
-    oa[i] = (uint32_t)(min(r8 + i * C::kRowStep, m_valid - 1) * lda + c8 * 16);
-  const int lds_st = swz(r8, c8);           // + i * kRowStep * 128 for load i
+  for (int i = 0; i < C::kLoadsPerWave; ++i) {
+    const int o = wave + i * C::kWaves;                 // wave-uniform
+    is_w[i] = o < C::BN / 8;
+    const int r = (is_w[i] ? o : o - C::BN / 8) * 8 + lrow;
+    goff[i] = is_w[i] ? (uint32_t)(min(r, n_valid - 1) * ldw + lchunk * 16)
+                      : (uint32_t)(min(r, m_valid - 1) * lda + lchunk * 16);
+  }
   const uint8_t* wbase = qw + n0 * ldw;
   const uint8_t* abase = qa + row_lo * lda;
 
-  uint4 rw[C::kWLoads];
-  uint4 ra[C::kALoads];
+  auto dma_stage = [&](int kb, int slot) {
+    uint8_t* sbase = lds + slot * C::kStageBytes;
+    const uint8_t* wb = wbase + kb * 128;
+    const uint8_t* ab = abase + kb * 128;
+#pragma unroll
+    for (int i = 0; i < C::kLoadsPerWave; ++i) {
+      const int o = wave + i * C::kWaves;
+      lds_dma16((is_w[i] ? wb : ab) + goff[i], sbase + o * 1024);
+    }
+  };
 
   // ---- scales: this lane's tokens (one per 16-row m sub-tile) and this wave's
-  //      128-row weight scale block
+  //      128-row weight scale block (a wave past N reads the last block and
+  //      stores nothing)
   uint32_t osa[C::TM];
 #pragma unroll
   for (int tm = 0; tm < C::TM; ++tm) osa[tm] = (uint32_t)min(wm * C::WTM + tm * 16 + (lane & 15), m_valid - 1);
   const float* sabase = sa + row_lo;
-  // a wave whose n range lies past N (tail tile) reads the last block's scales
-  // and stores nothing
   const float* swrow = sw + ((min(n0 + wn * C::WTN, N - 1) >> 7) * KB);
   const bool wave_active_n = wn * C::WTN < n_valid;
 
@@ -138,39 +172,35 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
   const int f0 = frow * 128 + (((2 * fg) ^ (frow & 7)) << 4);
   const int f1 = frow * 128 + (((2 * fg + 1) ^ (frow & 7)) << 4);
 
-  // prologue: K step 0 into stage 0
+  // prologue
+  float sa_cur[C::TM];
 #pragma unroll
-  for (int i = 0; i < C::kWLoads; ++i) rw[i] = *reinterpret_cast<const uint4*>(wbase + ow[i]);
+  for (int tm = 0; tm < C::TM; ++tm) sa_cur[tm] = sabase[osa[tm]];
+  float sw_cur = swrow[0];
 #pragma unroll
-  for (int i = 0; i < C::kALoads; ++i) ra[i] = *reinterpret_cast<const uint4*>(abase + oa[i]);
-#pragma unroll
-  for (int i = 0; i < C::kWLoads; ++i)
-    *reinterpret_cast<uint4*>(lds + lds_st + i * C::kRowStep * 128) = rw[i];
-#pragma unroll
-  for (int i = 0; i < C::kALoads; ++i)
-    *reinterpret_cast<uint4*>(lds + C::kWBytes + lds_st + i * C::kRowStep * 128) = ra[i];
-  __syncthreads();
+  for (int s = 0; s < C::STAGES - 1; ++s) dma_stage(min(s, KB - 1), s);
 
   for (int kb = 0; kb < KB; ++kb) {
-    // next K step's tiles into registers (the last step reloads itself; the
-    // copy then goes to the idle stage and is never read)
-    {
-      const int kn = min(kb + 1, KB - 1);
-      const uint8_t* wb = wbase + kn * 128;
-      const uint8_t* ab = abase + kn * 128;
-#pragma unroll
-      for (int i = 0; i < C::kWLoads; ++i) rw[i] = *reinterpret_cast<const uint4*>(wb + ow[i]);
-#pragma unroll
-      for (int i = 0; i < C::kALoads; ++i) ra[i] = *reinterpret_cast<const uint4*>(ab + oa[i]);
-    }
+    // step kb's DMA is the oldest still outstanding: STAGES-2 younger stages may stay in flight
+    wait_vmcnt<(C::STAGES - 2) * C::kLoadsPerWave>();
+    __syncthreads();
 
-    const float swv = swrow[kb];
-    const float* sak = sabase + (int64_t)kb * ld_sa;
+    // next step's scales (clamped: the last step reloads its own)
+    const int kn = min(kb + 1, KB - 1);
+    float sa_nxt[C::TM];
+    const float* sak = sabase + (int64_t)kn * ld_sa;
+#pragma unroll
+    for (int tm = 0; tm < C::TM; ++tm) sa_nxt[tm] = sak[osa[tm]];
+    const float sw_nxt = swrow[kn];
+
+    // refill the slot released by step kb-1 (past the end: reload the last step)
+    dma_stage(min(kb + C::STAGES - 1, KB - 1), (kb + C::STAGES - 1) % C::STAGES);
+
     float sc[C::TM];
 #pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sak[osa[tm]] * swv;
+    for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sa_cur[tm] * sw_cur;
 
-    const uint8_t* st = lds + (kb & 1) * C::kStageBytes;
+    const uint8_t* st = lds + (kb % C::STAGES) * C::kStageBytes;
     const uint8_t* sta = st + C::kWBytes + wm * C::WTM * 128;
     const uint8_t* stw = st + wn * C::WTN * 128;
     v8i32 bf[C::TM];
@@ -187,16 +217,12 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
       }
     }
 
-    {
-      uint8_t* sn = lds + ((kb + 1) & 1) * C::kStageBytes;
 #pragma unroll
-      for (int i = 0; i < C::kWLoads; ++i) *reinterpret_cast<uint4*>(sn + lds_st + i * C::kRowStep * 128) = rw[i];
-#pragma unroll
-      for (int i = 0; i < C::kALoads; ++i)
-        *reinterpret_cast<uint4*>(sn + C::kWBytes + lds_st + i * C::kRowStep * 128) = ra[i];
-    }
-    __syncthreads();
+    for (int tm = 0; tm < C::TM; ++tm) sa_cur[tm] = sa_nxt[tm];
+    sw_cur = sw_nxt;
   }
+  // drain the trailing (redundant) DMA before the workgroup may exit
+  wait_vmcnt<0>();
 
   // ---- epilogue: fp32 -> bf16 (RNE), four consecutive n per lane
   if (!wave_active_n) return;
