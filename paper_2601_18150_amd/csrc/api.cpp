@@ -4,7 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/fp8rl.h"
+#include "fp8rl.h"
 #include "launch.hpp"
 
 namespace {

@@ -15,15 +15,38 @@ using CfgLarge = GemmCfg<256, 256, 2, 4, 2>;   // 512 threads, wave tile 128(n) 
 using CfgMid = GemmCfg<256, 128, 2, 2, 3>;     // 256 threads, wave tile 128 x 64, 144 KiB LDS
 using CfgSmall = GemmCfg<128, 128, 2, 2, 3>;   // 256 threads, wave tile 64 x 64, 96 KiB LDS
 
+constexpr int kXcds = 8;        // MI355X: workgroup i is dispatched to XCD i % 8
+constexpr int kGroupM = 8;      // m tiles per band of the grouped raster order
+
+// Workgroup id -> output tile (encoded tile_n * tiles_m + tile_m).
+// 1. Renumber so that the workgroups one XCD receives (ids x, x+8, x+16, ...)
+//    walk one contiguous range of tile numbers.
+// 2. Walk tile numbers in bands of kGroupM m tiles, m fastest: the tiles an XCD
+//    runs at the same time share a few A row blocks and W row blocks, which
+//    then stay in that XCD's L2.
+__device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n) {
+  const int total = tiles_m * tiles_n;
+  const int q = total / kXcds, r = total % kXcds;
+  const int x = id % kXcds, j = id / kXcds;
+  const int t = x * q + min(x, r) + j;
+  const int band = t / (kGroupM * tiles_n);
+  const int first_m = band * kGroupM;
+  const int gm = min(tiles_m - first_m, kGroupM);
+  const int in_band = t - band * kGroupM * tiles_n;
+  const int tile_m = first_m + in_band % gm;
+  const int tile_n = in_band / gm;
+  return tile_n * tiles_m + tile_m;
+}
+
 template <class C>
 __global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_kernel(
     const uint8_t* __restrict__ qa, int64_t lda, const float* __restrict__ sa, int64_t ld_sa,
     const uint8_t* __restrict__ qw, int64_t ldw, const float* __restrict__ sw,
     uint16_t* __restrict__ y, int64_t ldy, int64_t M, int64_t N, int KB, int tiles_m) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
-  const int id = blockIdx.x;
-  const int tile_m = id % tiles_m;
-  const int tile_n = id / tiles_m;
+  const int tile = xcd_grouped_tile(blockIdx.x, tiles_m, (int)gridDim.x / tiles_m);
+  const int tile_m = tile % tiles_m;
+  const int tile_n = tile / tiles_m;
   const int64_t row_lo = (int64_t)tile_m * C::BM;
   const int64_t row_hi = min(row_lo + C::BM, M);
   gemm_tile<C>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, row_lo, row_hi, (int64_t)tile_n * C::BN, N, KB,

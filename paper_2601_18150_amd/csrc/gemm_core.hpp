@@ -45,11 +45,15 @@ struct GemmCfg {
   static constexpr int TM = WTM / 16;       // ... along m
   static constexpr int kWBytes = BN * 128;  // one K step of the W tile
   static constexpr int kABytes = BM * 128;
-  static constexpr int kStageBytes = kWBytes + kABytes;
+  static constexpr int kSBytes = BM * 4;    // one K step of the activation scales
+  static constexpr int kStageBytes = kWBytes + kABytes + kSBytes;
   static constexpr int kLdsBytes = STAGES * kStageBytes;
   // one direct-to-LDS wave instruction moves 8 rows x 128 bytes (1 KiB)
   static constexpr int kOctets = (BN + BM) / 8;
   static constexpr int kLoadsPerWave = kOctets / kWaves;
+  // activation scales: 64 tokens (one dword each) per wave instruction
+  static constexpr int kScaleLoads = BM / 64;
+  static_assert(BM % 64 == 0 && kScaleLoads <= kWaves, "one scale DMA per wave at most");
   static_assert(WTN % 16 == 0 && WTM % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(WTN <= 128 && 128 % WTN == 0, "a wave's n range must sit inside one 128-row scale block");
   static_assert(kOctets % kWaves == 0, "row octets must divide evenly among the waves");
@@ -57,8 +61,16 @@ struct GemmCfg {
   static_assert(kLdsBytes <= 160 * 1024, "LDS is 160 KiB per CU");
 };
 
-// Byte offset of 16-byte chunk `c` of row `r` in a swizzled 128-byte-row tile.
-__device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ (r & 7)) << 4); }
+// LDS tile layout: rows of 128 bytes (one K step), eight 16-byte chunks per
+// row; logical chunk c of row r is stored at physical chunk c ^ swz_key(r).
+// A fragment read (ds_read_b128) has 16 lanes reading the same logical chunk
+// of 16 consecutive rows.  With 64 banks of 4 bytes, row r's physical chunk p
+// lands on banks 32 (r & 1) + 4p .. +3, so the 16 rows need distinct
+// (r & 1, p): the key below is a permutation of 0..7 over the even rows and
+// over the odd rows of any 16-row group (and over any 8 consecutive rows,
+// which also keeps a 32-bank LDS conflict-free).
+__device__ __forceinline__ int swz_key(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int swz(int r, int c) { return r * 128 + ((c ^ swz_key(r)) << 4); }
 
 // 32-byte MFMA operand of one lane: two 16-byte chunks at byte offsets o0, o1.
 __device__ __forceinline__ v8i32 lds_frag2(const uint8_t* base, int o0, int o1) {
@@ -87,6 +99,12 @@ __device__ __forceinline__ void lds_dma16(const uint8_t* gptr, uint8_t* lds_wave
   __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 16, 0, 0);
 }
 
+// 4 bytes per lane, global -> LDS (global_load_lds_dword): lane L writes
+// LDS bytes [lds_wave_base + 4 L, +4).
+__device__ __forceinline__ void lds_dma4(const float* gptr, uint8_t* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 4, 0, 0);
+}
+
 // s_waitcnt vmcnt(n) only (expcnt and lgkmcnt left at their maxima)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -103,8 +121,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 //   prologue: DMA K steps 0 .. STAGES-2
 //   step kb:  wait for this wave's DMA of step kb; barrier (all waves' DMA of
 //             step kb landed, all waves done reading step kb-1's slot);
-//             prefetch next step's scales; DMA step kb+STAGES-1 into the slot
-//             freed by step kb-1; MFMA + scale-FMA on slot kb % STAGES.
+//             MFMA + scale-FMA on slot kb % STAGES, with the DMA of step
+//             kb+STAGES-1 into the slot freed by step kb-1 interleaved.
+// A slot holds the W tile, the A tile and the tile's BM activation scales of
+// one K step; the weight scale is a wave-uniform scalar load.  The DMA is then
+// the only vector-memory traffic of the loop, so the one explicit vmcnt wait
+// per step is the only wait on global memory.
 template <class C>
 __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_t lda,
                                           const float* __restrict__ sa, int64_t ld_sa,
@@ -123,9 +145,8 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
 
   // ---- DMA plan: wave w moves row octets w, w + kWaves, ...  In an octet,
   //      lane L lands at row 8o + (L >> 3), physical chunk (L & 7), which holds
-  //      logical chunk (L & 7) ^ (row & 7) of the swizzled layout.
+  //      logical chunk (L & 7) ^ swz_key(row) of the swizzled layout.
   const int lrow = lane >> 3;
-  const int lchunk = (lane & 7) ^ lrow;
   uint32_t goff[C::kLoadsPerWave];
   bool is_w[C::kLoadsPerWave];
 #pragma unroll
@@ -133,12 +154,20 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
     const int o = wave + i * C::kWaves;                 // wave-uniform
     is_w[i] = o < C::BN / 8;
     const int r = (is_w[i] ? o : o - C::BN / 8) * 8 + lrow;
+    const int lchunk = (lane & 7) ^ swz_key(r);
     goff[i] = is_w[i] ? (uint32_t)(min(r, n_valid - 1) * ldw + lchunk * 16)
                       : (uint32_t)(min(r, m_valid - 1) * lda + lchunk * 16);
   }
   const uint8_t* wbase = qw + n0 * ldw;
   const uint8_t* abase = qa + row_lo * lda;
 
+  // ---- scales: wave w < kScaleLoads DMAs tokens 64w .. 64w+63 of the tile
+  //      (clamped to the last valid row); this wave's 128-row weight scale
+  //      block is read with scalar loads (a wave past N reads the last block
+  //      and stores nothing)
+  const bool sdma = wave < C::kScaleLoads;
+  const float* sa_lane = sa + row_lo + min(wave * 64 + lane, m_valid - 1);
+  const float* swrow = sw + ((min(n0 + wn * C::WTN, N - 1) >> 7) * KB);
   auto dma_stage = [&](int kb, int slot) {
     uint8_t* sbase = lds + slot * C::kStageBytes;
     const uint8_t* wb = wbase + kb * 128;
@@ -148,16 +177,9 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
       const int o = wave + i * C::kWaves;
       lds_dma16((is_w[i] ? wb : ab) + goff[i], sbase + o * 1024);
     }
+    if (sdma) lds_dma4(sa_lane + (int64_t)kb * ld_sa, sbase + C::kWBytes + C::kABytes + wave * 256);
   };
 
-  // ---- scales: this lane's tokens (one per 16-row m sub-tile) and this wave's
-  //      128-row weight scale block (a wave past N reads the last block and
-  //      stores nothing)
-  uint32_t osa[C::TM];
-#pragma unroll
-  for (int tm = 0; tm < C::TM; ++tm) osa[tm] = (uint32_t)min(wm * C::WTM + tm * 16 + (lane & 15), m_valid - 1);
-  const float* sabase = sa + row_lo;
-  const float* swrow = sw + ((min(n0 + wn * C::WTN, N - 1) >> 7) * KB);
   const bool wave_active_n = wn * C::WTN < n_valid;
 
   v4f32 acc[C::TN][C::TM];
@@ -169,57 +191,74 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
   const int frow = lane & 15;
   const int fg = lane >> 4;
   // fragment byte offsets inside a tile: row frow (+16 per sub-tile), chunks 2g, 2g+1
-  const int f0 = frow * 128 + (((2 * fg) ^ (frow & 7)) << 4);
-  const int f1 = frow * 128 + (((2 * fg + 1) ^ (frow & 7)) << 4);
+  // (sub-tiles start at multiples of 16 rows, so swz_key(row) = swz_key(frow))
+  const int f0 = swz(frow, 2 * fg);
+  const int f1 = swz(frow, 2 * fg + 1);
 
   // prologue
-  float sa_cur[C::TM];
-#pragma unroll
-  for (int tm = 0; tm < C::TM; ++tm) sa_cur[tm] = sabase[osa[tm]];
-  float sw_cur = swrow[0];
 #pragma unroll
   for (int s = 0; s < C::STAGES - 1; ++s) dma_stage(min(s, KB - 1), s);
 
   for (int kb = 0; kb < KB; ++kb) {
-    // step kb's DMA is the oldest still outstanding: STAGES-2 younger stages may stay in flight
-    wait_vmcnt<(C::STAGES - 2) * C::kLoadsPerWave>();
+    // step kb's DMA is the oldest still outstanding: STAGES-2 younger stages
+    // (kLoadsPerWave tile loads + at most one scale load each) may stay in flight
+    if (sdma)
+      wait_vmcnt<(C::STAGES - 2) * (C::kLoadsPerWave + 1)>();
+    else
+      wait_vmcnt<(C::STAGES - 2) * C::kLoadsPerWave>();
     __syncthreads();
 
-    // next step's scales (clamped: the last step reloads its own)
-    const int kn = min(kb + 1, KB - 1);
-    float sa_nxt[C::TM];
-    const float* sak = sabase + (int64_t)kn * ld_sa;
-#pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm) sa_nxt[tm] = sak[osa[tm]];
-    const float sw_nxt = swrow[kn];
+    // refill the slot released by step kb-1 (past the end: reload the last
+    // step); the DMA instructions are spread over the first half of the
+    // sub-tile loop below: issued all at once they stall the wave on a full
+    // address queue, issued late they arrive after the next barrier
+    const int kd = min(kb + C::STAGES - 1, KB - 1);
+    uint8_t* dslot = lds + ((kb + C::STAGES - 1) % C::STAGES) * C::kStageBytes;
+    const uint8_t* dwb = wbase + kd * 128;
+    const uint8_t* dab = abase + kd * 128;
 
-    // refill the slot released by step kb-1 (past the end: reload the last step)
-    dma_stage(min(kb + C::STAGES - 1, KB - 1), (kb + C::STAGES - 1) % C::STAGES);
-
+    constexpr int kDmaSpread = C::TN >= 4 ? C::TN / 2 : C::TN;   // sub-tiles that carry DMA issue
+    const uint8_t* st = lds + (kb % C::STAGES) * C::kStageBytes;
+    const float* sts = reinterpret_cast<const float*>(st + C::kWBytes + C::kABytes) + wm * C::WTM + (lane & 15);
+    const float swv = swrow[kb];
     float sc[C::TM];
 #pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sa_cur[tm] * sw_cur;
+    for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sts[tm * 16] * swv;
 
-    const uint8_t* st = lds + (kb % C::STAGES) * C::kStageBytes;
     const uint8_t* sta = st + C::kWBytes + wm * C::WTM * 128;
     const uint8_t* stw = st + wn * C::WTN * 128;
+    // first weight fragment, then the activation fragments in the order the
+    // first MFMAs consume them (LDS returns in order, so each MFMA waits only
+    // for its own operands); weight fragments are double-buffered: the next
+    // sub-tile's read is in flight while this one's MFMAs run
+    v8i32 af = lds_frag2(stw, f0, f1);
     v8i32 bf[C::TM];
 #pragma unroll
     for (int tm = 0; tm < C::TM; ++tm) bf[tm] = lds_frag2(sta + tm * 16 * 128, f0, f1);
 #pragma unroll
     for (int tn = 0; tn < C::TN; ++tn) {
-      const v8i32 af = lds_frag2(stw + tn * 16 * 128, f0, f1);
 #pragma unroll
-      for (int tm = 0; tm < C::TM; ++tm) {
-        const v4f32 p = mfma_fp8_16x16x128(af, bf[tm]);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[tn][tm][r] = __builtin_fmaf(p[r], sc[tm], acc[tn][tm][r]);
+      for (int i = 0; i < C::kLoadsPerWave; ++i) {
+        if ((i * kDmaSpread) / C::kLoadsPerWave == tn) {
+          const int o = wave + i * C::kWaves;
+          lds_dma16((is_w[i] ? dwb : dab) + goff[i], dslot + o * 1024);
+        }
       }
+      if (tn == 0 && sdma) lds_dma4(sa_lane + (int64_t)kd * ld_sa, dslot + C::kWBytes + C::kABytes + wave * 256);
+      v8i32 af_next = af;
+      if (tn + 1 < C::TN) af_next = lds_frag2(stw + (tn + 1) * 16 * 128, f0, f1);
+      // all MFMAs of the sub-tile row first (independent results in flight),
+      // then their scale FMAs
+      v4f32 p[C::TM];
+#pragma unroll
+      for (int tm = 0; tm < C::TM; ++tm) p[tm] = mfma_fp8_16x16x128(af, bf[tm]);
+#pragma unroll
+      for (int tm = 0; tm < C::TM; ++tm)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[tn][tm][r] = __builtin_fmaf(p[tm][r], sc[tm], acc[tn][tm][r]);
+      af = af_next;
     }
 
-#pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm) sa_cur[tm] = sa_nxt[tm];
-    sw_cur = sw_nxt;
   }
   // drain the trailing (redundant) DMA before the workgroup may exit
   wait_vmcnt<0>();
