@@ -86,7 +86,7 @@ int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld
   if (num_groups < 1) return FP8RL_ERR_INVALID_ARG;
   if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (total_rows >= kMaxDim || n >= kMaxDim || k >= kMaxDim || num_groups >= (int64_t(1) << 20) ||
-      n / 128 > 65535)
+      (total_rows / 128 + num_groups) * (n / 128) >= (int64_t(1) << 31))
     return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (total_rows == 0 || n == 0) return FP8RL_OK;
   if (!qa || !sa || !qw || !sw || !group_offsets || !y) return FP8RL_ERR_INVALID_ARG;

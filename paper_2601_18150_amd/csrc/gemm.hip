@@ -11,9 +11,12 @@ namespace fp8rl {
 namespace {
 
 // Tile configurations.
-using CfgLarge = GemmCfg<256, 256, 2, 4, 2>;   // 512 threads, wave tile 128(n) x 64(m), 128 KiB LDS
-using CfgMid = GemmCfg<256, 128, 2, 2, 3>;     // 256 threads, wave tile 128 x 64, 144 KiB LDS
-using CfgSmall = GemmCfg<128, 128, 2, 2, 3>;   // 256 threads, wave tile 64 x 64, 96 KiB LDS
+// (measured on MI355X: 256x128 tiles with 3 slots and 128x128 tiles with 3
+// slots were both slower than these two on every configured shape; 128x128
+// with 2 slots fits two workgroups per CU, which is what small-M and MoE
+// shapes need to fill the 256 CUs)
+using CfgLarge = GemmCfg<256, 256, 2, 4, 2>;   // 512 threads, wave tile 128(n) x 64(m), 130 KiB LDS
+using CfgSmall = GemmCfg<128, 128, 2, 2, 2>;   // 256 threads, wave tile 64 x 64, 65 KiB LDS
 
 constexpr int kXcds = 8;        // MI355X: workgroup i is dispatched to XCD i % 8
 constexpr int kGroupM = 8;      // m tiles per band of the grouped raster order
@@ -24,11 +27,16 @@ constexpr int kGroupM = 8;      // m tiles per band of the grouped raster order
 // 2. Walk tile numbers in bands of kGroupM m tiles, m fastest: the tiles an XCD
 //    runs at the same time share a few A row blocks and W row blocks, which
 //    then stay in that XCD's L2.
-__device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n) {
-  const int total = tiles_m * tiles_n;
+// Renumber workgroup ids so that the ids one XCD receives (x, x+8, x+16, ...)
+// map to one contiguous range of [0, total).
+__device__ __forceinline__ int xcd_contiguous(int id, int total) {
   const int q = total / kXcds, r = total % kXcds;
   const int x = id % kXcds, j = id / kXcds;
-  const int t = x * q + min(x, r) + j;
+  return x * q + min(x, r) + j;
+}
+
+__device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n) {
+  const int t = xcd_contiguous(id, tiles_m * tiles_n);
   const int band = t / (kGroupM * tiles_n);
   const int first_m = band * kGroupM;
   const int gm = min(tiles_m - first_m, kGroupM);
@@ -53,19 +61,25 @@ __global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_kernel(
                lds);
 }
 
-// Grouped GEMM: blockIdx.y = n tile, blockIdx.x = m tile counted over all
-// experts in order (expert e owns ceil(rows_e / BM) consecutive m tiles).  The
-// grid is sized for the worst case (total_rows / BM + num_groups); workgroups
-// past the last real tile exit at once.
+// Grouped GEMM: a 1-D grid of max_tiles_m x tiles_n workgroups.  The m tile
+// index counts over all experts in order (expert e owns ceil(rows_e / BM)
+// consecutive m tiles); the grid is sized for the worst case
+// (total_rows / BM + num_groups) and workgroups past the last real tile exit at
+// once.  Ids are renumbered so that each XCD walks a contiguous range, m tile
+// fastest: the m tiles of one expert that share a weight slab run on the same
+// XCD and read it from its L2.
 template <class C>
 __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
     const uint8_t* __restrict__ qa, const float* __restrict__ sa, int64_t ld_sa,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw,
-    const int32_t* __restrict__ offsets, int G, uint16_t* __restrict__ y, int64_t N, int64_t K) {
+    const int32_t* __restrict__ offsets, int G, uint16_t* __restrict__ y, int64_t N, int64_t K,
+    int max_tiles_m) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
   __shared__ int found[2];
   const int t = threadIdx.x;
-  const int target = blockIdx.x;
+  const int lin = xcd_contiguous(blockIdx.x, (int)gridDim.x);
+  const int target = lin % max_tiles_m;
+  const int tile_n = lin / max_tiles_m;
   if (t == 0) found[0] = -1;
   __syncthreads();
   if (t < 64) {
@@ -98,7 +112,7 @@ __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
   const int64_t row_lo = (int64_t)offsets[e] + (int64_t)mt * C::BM;
   const int64_t row_hi = min(row_lo + C::BM, (int64_t)offsets[e + 1]);
   gemm_tile<C>(qa, K, sa, ld_sa, qw + (int64_t)e * N * K, K, sw + (int64_t)e * (N / 128) * KB, y, N,
-               row_lo, row_hi, (int64_t)blockIdx.y * C::BN, N, KB, lds);
+               row_lo, row_hi, (int64_t)tile_n * C::BN, N, KB, lds);
 }
 
 template <class C>
@@ -117,9 +131,10 @@ hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, con
                           const float* sw, const int32_t* offsets, int64_t g, int64_t rows, uint16_t* y,
                           int64_t n, int64_t k, hipStream_t stream) {
   const int64_t max_tiles_m = rows / C::BM + g;
-  const int tiles_n = (int)((n + C::BN - 1) / C::BN);
-  hipLaunchKernelGGL(grouped_gemm_w8a8_block_kernel<C>, dim3((unsigned)max_tiles_m, (unsigned)tiles_n),
-                     dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw, sw, offsets, (int)g, y, n, k);
+  const int64_t tiles_n = (n + C::BN - 1) / C::BN;
+  hipLaunchKernelGGL(grouped_gemm_w8a8_block_kernel<C>, dim3((unsigned)(max_tiles_m * tiles_n)),
+                     dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw, sw, offsets, (int)g, y, n, k,
+                     (int)max_tiles_m);
   return hipGetLastError();
 }
 
@@ -130,8 +145,6 @@ hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* s
                                   int64_t m, int64_t n, int64_t k, hipStream_t stream) {
   if (m >= 2048 && n >= 2048)
     return launch_dense<CfgLarge>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
-  if (m > 128)
-    return launch_dense<CfgMid>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
   return launch_dense<CfgSmall>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
 }
 
