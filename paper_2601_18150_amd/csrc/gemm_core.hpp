@@ -197,22 +197,29 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
 
   // prologue
 #pragma unroll
-  for (int s = 0; s < C::STAGES - 1; ++s) dma_stage(min(s, KB - 1), s);
+  for (int s = 0; s < C::STAGES - 1; ++s)
+    if (s < KB) dma_stage(s, s);
 
   for (int kb = 0; kb < KB; ++kb) {
-    // step kb's DMA is the oldest still outstanding: STAGES-2 younger stages
-    // (kLoadsPerWave tile loads + at most one scale load each) may stay in flight
-    if (sdma)
-      wait_vmcnt<(C::STAGES - 2) * (C::kLoadsPerWave + 1)>();
-    else
-      wait_vmcnt<(C::STAGES - 2) * C::kLoadsPerWave>();
+    // step kb's DMA is the oldest still outstanding: up to STAGES-2 younger
+    // stages (kLoadsPerWave tile loads + at most one scale load each) may stay
+    // in flight; near the end of K fewer were issued, so wait for everything
+    if (kb + C::STAGES - 2 < KB) {
+      if (sdma)
+        wait_vmcnt<(C::STAGES - 2) * (C::kLoadsPerWave + 1)>();
+      else
+        wait_vmcnt<(C::STAGES - 2) * C::kLoadsPerWave>();
+    } else {
+      wait_vmcnt<0>();
+    }
     __syncthreads();
 
-    // refill the slot released by step kb-1 (past the end: reload the last
-    // step); the DMA instructions are spread over the first half of the
-    // sub-tile loop below: issued all at once they stall the wave on a full
-    // address queue, issued late they arrive after the next barrier
-    const int kd = min(kb + C::STAGES - 1, KB - 1);
+    // refill the slot released by step kb-1 with step kb+STAGES-1 (none past
+    // the end of K); the DMA instructions are spread over the first half of
+    // the sub-tile loop below: issued all at once they stall the wave on a
+    // full address queue, issued late they arrive after the next barrier
+    const bool refill = kb + C::STAGES - 1 < KB;
+    const int kd = min(kb + C::STAGES - 1, KB - 1);   // (only used when refill)
     uint8_t* dslot = lds + ((kb + C::STAGES - 1) % C::STAGES) * C::kStageBytes;
     const uint8_t* dwb = wbase + kd * 128;
     const uint8_t* dab = abase + kd * 128;
@@ -239,12 +246,12 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
     for (int tn = 0; tn < C::TN; ++tn) {
 #pragma unroll
       for (int i = 0; i < C::kLoadsPerWave; ++i) {
-        if ((i * kDmaSpread) / C::kLoadsPerWave == tn) {
+        if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill) {
           const int o = wave + i * C::kWaves;
           lds_dma16((is_w[i] ? dwb : dab) + goff[i], dslot + o * 1024);
         }
       }
-      if (tn == 0 && sdma) lds_dma4(sa_lane + (int64_t)kd * ld_sa, dslot + C::kWBytes + C::kABytes + wave * 256);
+      if (tn == 0 && sdma && refill) lds_dma4(sa_lane + (int64_t)kd * ld_sa, dslot + C::kWBytes + C::kABytes + wave * 256);
       v8i32 af_next = af;
       if (tn + 1 < C::TN) af_next = lds_frag2(stw + (tn + 1) * 16 * 128, f0, f1);
       // all MFMAs of the sub-tile row first (independent results in flight),
@@ -260,8 +267,7 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
     }
 
   }
-  // drain the trailing (redundant) DMA before the workgroup may exit
-  wait_vmcnt<0>();
+  // (the last iteration waited for every DMA: nothing is in flight here)
 
   // ---- epilogue: fp32 -> bf16 (RNE), four consecutive n per lane
   if (!wave_active_n) return;
