@@ -135,9 +135,9 @@ def prefill(args, fp8rl):
                    "weight_block": [128, 128], "act_group": [1, 128], "seed": args.seed},
         "roofline": {
             "bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": gemm_traffic_bytes(),
             "kernel": "gemm_w8a8_block", "avg_ms": round(kern["gemm"], 5),
-            "algorithmic_flops_per_launch": flops,
+            "algorithmic_flops_per_launch": flops, "traffic_unit": "HBM bytes per launch",
         },
         "kernels": {
             "quant_weight_block128": {"avg_ms": round(kern["quant_weight"], 5),
@@ -262,7 +262,30 @@ def moe(args, fp8rl, steps=10, warmup=3):
 # ---------------------------------------------------------------------------
 # CPU oracle baseline on a bounded sample of the prefill step
 # ---------------------------------------------------------------------------
-def cpu_baseline(a, w, rows=16):
+GEMM_SOURCES = ["gemm_core.hpp", "gemm.hip", "common.hpp"]
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_prefill_gate_up_traffic.md")
+
+
+def gemm_traffic_bytes():
+    """HBM bytes per GEMM launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
+    (calibrated on a device copy), read from the committed profile summary; None
+    when the GEMM sources changed since it was taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2601_18150_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    fields = dict(ln.split(":", 1) for ln in text.splitlines() if ln.startswith(("hbm_bytes_per_launch:", "source_sha256:")))
+    if fields.get("source_sha256", "").strip() != h.hexdigest()[:16]:
+        return None
+    return int(fields["hbm_bytes_per_launch"].strip())
+
+
+def cpu_baseline(a, w, rows=2048):
     import numpy as np
     from oracle import gemm, quant
     try:
