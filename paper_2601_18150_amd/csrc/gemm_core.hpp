@@ -50,15 +50,15 @@ struct GemmCfg {
   static constexpr int kLdsBytes = STAGES * kStageBytes;
   // one direct-to-LDS wave instruction moves 8 rows x 128 bytes (1 KiB)
   static constexpr int kOctets = (BN + BM) / 8;
-  static constexpr int kLoadsPerWave = (kOctets + kWaves - 1) / kWaves;   // the last may be partial
+  static constexpr int kLoadsPerWave = kOctets / kWaves;
   // activation scales: 64 tokens (one dword each) per wave instruction
   static constexpr int kScaleLoads = BM / 64;
   static_assert(BM % 64 == 0 && kScaleLoads <= kWaves, "one scale DMA per wave at most");
   static_assert(WTN % 16 == 0 && WTM % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(WTN <= 128 && 128 % WTN == 0, "a wave's n range must sit inside one 128-row scale block");
-  // with more than two slots the per-step vmcnt wait assumes every wave issues
-  // the same number of DMA instructions
-  static_assert(kOctets % kWaves == 0 || STAGES == 2, "uneven DMA split needs exactly two slots");
+  // the per-step vmcnt wait assumes every wave issues the same number of DMA
+  // instructions
+  static_assert(kOctets % kWaves == 0, "row octets must divide evenly among the waves");
   static_assert(STAGES >= 2, "need at least double buffering");
   static_assert(kLdsBytes <= 160 * 1024, "LDS is 160 KiB per CU");
 };
@@ -177,7 +177,7 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
 #pragma unroll
     for (int i = 0; i < C::kLoadsPerWave; ++i) {
       const int o = wave + i * C::kWaves;
-      if (o < C::kOctets) lds_dma16((is_w[i] ? wb : ab) + goff[i], sbase + o * 1024);
+      lds_dma16((is_w[i] ? wb : ab) + goff[i], sbase + o * 1024);
     }
     if (sdma) lds_dma4(sa_lane + (int64_t)kb * ld_sa, sbase + C::kWBytes + C::kABytes + wave * 256);
   };
@@ -249,7 +249,7 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
 #pragma unroll
       for (int i = 0; i < C::kLoadsPerWave; ++i) {
         const int o = wave + i * C::kWaves;
-        if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill && o < C::kOctets) {
+        if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill) {
           lds_dma16((is_w[i] ? dwb : dab) + goff[i], dslot + o * 1024);
         }
       }
