@@ -56,8 +56,6 @@ struct GemmCfg {
   static_assert(BM % 64 == 0 && kScaleLoads <= kWaves, "one scale DMA per wave at most");
   static_assert(WTN % 16 == 0 && WTM % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(WTN <= 128 && 128 % WTN == 0, "a wave's n range must sit inside one 128-row scale block");
-  // the per-step vmcnt wait assumes every wave issues the same number of DMA
-  // instructions
   static_assert(kOctets % kWaves == 0, "row octets must divide evenly among the waves");
   static_assert(STAGES >= 2, "need at least double buffering");
   static_assert(kLdsBytes <= 160 * 1024, "LDS is 160 KiB per CU");
@@ -248,8 +246,8 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
     for (int tn = 0; tn < C::TN; ++tn) {
 #pragma unroll
       for (int i = 0; i < C::kLoadsPerWave; ++i) {
-        const int o = wave + i * C::kWaves;
         if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill) {
+          const int o = wave + i * C::kWaves;
           lds_dma16((is_w[i] ? dwb : dab) + goff[i], dslot + o * 1024);
         }
       }
