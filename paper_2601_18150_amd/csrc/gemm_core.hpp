@@ -3,7 +3,7 @@
 // Computes one BN x BM output tile of  Y^T = W . A^T  over the whole K range:
 // the weight tile provides the MFMA "A" operand (16 rows of n per instruction)
 // and the activation tile the "B" operand (16 rows of m), so each lane's four
-// fp32 results are four consecutive n of one token m -- an 8-byte bf16 store.
+// fp32 results are four consecutive n of one token m.
 //
 // K is walked in 128-wide steps, one per scale block (section 2.1.1: weight
 // scales per 128x128 block, activation scales per 1x128 group).  A single
@@ -16,8 +16,9 @@
 // Data movement per K step: the block's W and A tiles (BN x 128 and BM x 128
 // bytes) go straight from global memory into an LDS ring (global_load_lds,
 // no register staging), rows of 128 bytes with the 16-byte chunk index
-// XOR-swizzled by (row & 7) so that the fragment reads (ds_read_b128) of 8
-// consecutive rows hit 8 distinct bank groups.
+// XOR-swizzled so that the fragment reads (ds_read_b128) are free of bank
+// conflicts.  The finished tile is converted to bf16, staged in LDS and written
+// as whole output rows.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -105,6 +106,13 @@ __device__ __forceinline__ void lds_dma4(const float* gptr, uint8_t* lds_wave_ba
   __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 4, 0, 0);
 }
 
+// 16-byte streaming (non-temporal) store of eight bf16
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void store_stream16(uint16_t* p, const uint4& v) {
+  const u32x4_t w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t*>(p));
+}
+
 // s_waitcnt vmcnt(n) only (expcnt and lgkmcnt left at their maxima)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -179,8 +187,6 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
     }
     if (sdma) lds_dma4(sa_lane + (int64_t)kb * ld_sa, sbase + C::kWBytes + C::kABytes + wave * 256);
   };
-
-  const bool wave_active_n = wn * C::WTN < n_valid;
 
   v4f32 acc[C::TN][C::TM];
 #pragma unroll
@@ -269,20 +275,38 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
   }
   // (the last iteration waited for every DMA: nothing is in flight here)
 
-  // ---- epilogue: fp32 -> bf16 (RNE), four consecutive n per lane
-  if (!wave_active_n) return;
+  // ---- epilogue: fp32 -> bf16 (RNE) into a copy of the whole tile in LDS (the
+  //      ring is free once every wave is past its last K step), then each
+  //      workgroup writes full 16-byte chunks of whole output rows with
+  //      streaming stores.  Direct 8-byte stores from the MFMA layout wrote
+  //      partial cache lines (1.6x the output bytes reached HBM) and let the
+  //      output displace the operands in the memory-side cache.
+  //      LDS layout: BM rows of BN bf16; 16-byte chunk c of row r sits at
+  //      c ^ (r & 15), so the 16 rows of one fragment store, and the two rows
+  //      of one read-back wave instruction, spread evenly over the 64 banks.
+  constexpr int kRowBytes = C::BN * 2;
+  constexpr int kChunks = kRowBytes / 16;
+  static_assert(kChunks >= 16 && C::BM * kRowBytes <= C::kLdsBytes, "the bf16 tile must fit in the LDS ring");
+  __syncthreads();
 #pragma unroll
   for (int tn = 0; tn < C::TN; ++tn) {
     const int nl = wn * C::WTN + tn * 16 + 4 * fg;
-    if (nl >= n_valid) continue;
 #pragma unroll
     for (int tm = 0; tm < C::TM; ++tm) {
       const int ml = wm * C::WTM + tm * 16 + frow;
-      if (ml >= m_valid) continue;
       uint2 o;
       o.x = f32_to_bf16_rne(acc[tn][tm][0]) | (f32_to_bf16_rne(acc[tn][tm][1]) << 16);
       o.y = f32_to_bf16_rne(acc[tn][tm][2]) | (f32_to_bf16_rne(acc[tn][tm][3]) << 16);
-      *reinterpret_cast<uint2*>(y + (row_lo + ml) * ldy + n0 + nl) = o;
+      *reinterpret_cast<uint2*>(lds + ml * kRowBytes + (((nl >> 3) ^ (ml & 15)) << 4) + ((nl >> 2) & 1) * 8) = o;
+    }
+  }
+  __syncthreads();
+  const int c = t % kChunks;                    // this thread's chunk of every row it writes
+#pragma unroll 4
+  for (int r = t / kChunks; r < C::BM; r += C::kThreads / kChunks) {
+    if (r < m_valid && c * 8 < n_valid) {
+      const uint4 v = *reinterpret_cast<const uint4*>(lds + r * kRowBytes + ((c ^ (r & 15)) << 4));
+      store_stream16(y + (row_lo + r) * ldy + n0 + c * 8, v);
     }
   }
 }
