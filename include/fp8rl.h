@@ -100,7 +100,8 @@ int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int6
  * y   [m][ldy] bf16 out
  * fp32 accumulation inside each 128-wide K block, fp32 scale application per K
  * block, fp32 -> bf16 round-to-nearest-even at the end; no bias.
- * n, k multiples of 128; m >= 0 arbitrary (m == 0 is a no-op).
+ * n, k multiples of 128; m >= 0 arbitrary (m == 0 is a no-op); at most 2^30
+ * output tiles of 128 x 128 (ceil(m/128) * n/128), else FP8RL_ERR_UNSUPPORTED_SHAPE.
  * Alignment: qa, qw, y 16-byte aligned; lda % 16 == 0; ldw % 16 == 0; ldy % 8 == 0;
  * sa, sw 4-byte aligned.  lda >= k, ldw >= k, ldy >= n, ld_sa >= m.
  */

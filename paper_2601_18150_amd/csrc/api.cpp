@@ -68,6 +68,7 @@ int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64
   if (m < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
   if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (m >= kMaxDim || n >= kMaxDim || k >= kMaxDim) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (((m + 127) / 128) * (n / 128) >= (int64_t(1) << 30)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (m == 0 || n == 0) return FP8RL_OK;
   if (!qa || !sa || !qw || !sw || !y) return FP8RL_ERR_INVALID_ARG;
   if (k == 0) return FP8RL_ERR_UNSUPPORTED_SHAPE;   // an empty reduction is not a blockwise GEMM

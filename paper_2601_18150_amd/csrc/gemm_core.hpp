@@ -221,16 +221,18 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
     __syncthreads();
 
     // refill the slot released by step kb-1 with step kb+STAGES-1 (none past
-    // the end of K); the DMA instructions are spread over the first half of
-    // the sub-tile loop below: issued all at once they stall the wave on a
-    // full address queue, issued late they arrive after the next barrier
+    // the end of K).  With 8 sub-tile rows per wave the DMA instructions are
+    // spread over the first half of the sub-tile loop below (issued all at once
+    // they stall the wave on a full address queue, issued later they arrive
+    // after the next barrier); with fewer, all are issued with the first one
+    // (measured fastest for the 128x128 tiles).
     const bool refill = kb + C::STAGES - 1 < KB;
     const int kd = min(kb + C::STAGES - 1, KB - 1);   // (only used when refill)
     uint8_t* dslot = lds + ((kb + C::STAGES - 1) % C::STAGES) * C::kStageBytes;
     const uint8_t* dwb = wbase + kd * 128;
     const uint8_t* dab = abase + kd * 128;
 
-    constexpr int kDmaSpread = C::TN >= 4 ? C::TN / 2 : C::TN;   // sub-tiles that carry DMA issue
+    constexpr int kDmaSpread = C::TN >= 8 ? C::TN / 2 : 1;   // sub-tile rows that carry DMA issue
     const uint8_t* st = lds + (kb % C::STAGES) * C::kStageBytes;
     const float* sts = reinterpret_cast<const float*>(st + C::kWBytes + C::kABytes) + wm * C::WTM + (lane & 15);
     const float swv = swrow[kb];

@@ -87,6 +87,8 @@ def test_gemm_argument_errors(lib):
     assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, -8, 128, 128, None) == INVALID
     assert f(A16, 128, A16, 8, A16, 128, A16, A16, 200, 8, 200, 128, None) == SHAPE
     assert f(A16, 256, A16, 8, A16, 256, A16, A16, 128, 8, 128, 192, None) == SHAPE
+    big = 1 << 30                                                     # 2^46 output tiles
+    assert f(A16, 128, A16, big, A16, 128, A16, A16, big, big, big, 128, None) == SHAPE
     assert f(A16, 128, A16, 7, A16, 128, A16, A16, 128, 8, 128, 128, None) == INVALID  # ld_sa < m
     assert f(A16, 128, A16, 8, A16, 128, A16, A16, 120, 8, 128, 128, None) == INVALID  # ldy < n
     assert f(A16, 128, A16, 8, None, 128, A16, A16, 128, 8, 128, 128, None) == INVALID
