@@ -11,10 +11,12 @@ The JSON line's `value` is the step's effective GEMM throughput (2MNK per step
 / step time, TFLOP/s, all three kernels inside the timed region).  `roofline`
 is the GEMM kernel alone, timed with HIP events on the stream it runs on.
 `extra` carries the same run's weight-resync figure (36 Qwen3-8B layers, 144
-matrices, GB/s vs HBM) and the MoE grouped GEMM (Qwen3-30B-A3B experts).
+matrices, GB/s vs HBM), the MoE grouped GEMM (Qwen3-30B-A3B experts), the
+decode linears of one Qwen3-8B layer (M=256) and a plain device copy.
 `cpu_baseline` times the CPU oracle on a bounded row sample of the same step.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload prefill]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+                       [--workload prefill|requant|moe|decode|copy]
                        [--no-cpu-baseline] [--no-extra]
 """
 import argparse
@@ -40,7 +42,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe"])
+    ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe", "copy"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -260,6 +262,38 @@ def moe(args, fp8rl, steps=10, warmup=3):
 
 
 # ---------------------------------------------------------------------------
+# decode linears of one Qwen3-8B layer (M=256): GEMM timing per linear
+# ---------------------------------------------------------------------------
+def decode(args, fp8rl, steps=20, warmup=5):
+    acts = synth.decode_activations(device="cuda")
+    wts = synth.layer_weights(0, device="cuda")
+    res = {}
+    for name, (k, n) in synth.QWEN3_8B_LINEARS.items():
+        x = acts["h"] if k == 4096 else acts["inter"]
+        qa, sa = fp8rl.fp8rl_quant_act_token_group128(x)
+        qw, sw = fp8rl.fp8rl_quant_weight_block128(wts[name])
+        y = torch.empty((x.shape[0], n), dtype=torch.bfloat16, device="cuda")
+        timer = KernelTimer()
+
+        def step():
+            with timer.span("gemm"):
+                fp8rl.fp8rl_gemm_w8a8_block(qa, sa, qw, sw, y=y)
+
+        timed_loop(step, steps, warmup, timer)
+        kms = timer.averages_ms()["gemm"]
+        m = x.shape[0]
+        flops = 2.0 * m * n * k
+        nbytes = n * k + m * k + m * n * 2 + (n // 128) * (k // 128) * 4 + m * (k // 128) * 4
+        t = flops / (kms * 1e-3) / 1e12
+        gbs = nbytes / (kms * 1e-3) / 1e9
+        res[name] = {"M": m, "K": k, "N": n, "avg_ms": round(kms, 5), "TFLOP/s": round(t, 1),
+                     "frac_fp8_peak": round(t / FP8_PEAK_TFLOPS, 4), "GB/s_min_traffic": round(gbs, 1),
+                     "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+    res["layer_ms"] = round(sum(v["avg_ms"] for v in res.values()), 5)
+    return res
+
+
+# ---------------------------------------------------------------------------
 # CPU oracle baseline on a bounded sample of the prefill step
 # ---------------------------------------------------------------------------
 GEMM_SOURCES = ["gemm_core.hpp", "gemm.hip", "common.hpp"]
@@ -285,7 +319,10 @@ def gemm_traffic_bytes():
     return int(fields["hbm_bytes_per_launch"].strip())
 
 
-def cpu_baseline(a, w, rows=2048):
+def cpu_baseline(a, w, chunk=1024, min_seconds=10.0):
+    """The numpy oracle on the host, as a reported baseline: quantise all weights,
+    then quantise and multiply 1024-row chunks of the activations until
+    min_seconds have passed or all rows are done (the sample is stated)."""
     import numpy as np
     from oracle import gemm, quant
     try:
@@ -293,19 +330,24 @@ def cpu_baseline(a, w, rows=2048):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
         threads = len(os.sched_getaffinity(0))
-    a_s = a[:rows].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-    w_h = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-    t0 = time.perf_counter()
-    qw, sw = quant.quant_weight_block128(w_h)
-    qa, sa = quant.quant_act_token_group128(a_s)
-    gemm.gemm_ref_fp64(qa, sa, qw, sw)
-    dt = time.perf_counter() - t0
     m, k = a.shape
     n = w.shape[0]
+    w_h = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    a_h = a.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    t0 = time.perf_counter()
+    qw, sw = quant.quant_weight_block128(w_h)
+    rows = 0
+    while rows < m and (rows == 0 or time.perf_counter() - t0 < min_seconds):
+        r1 = min(rows + chunk, m)
+        qa, sa = quant.quant_act_token_group128(a_h[rows:r1])
+        gemm.gemm_ref_fp64(qa, sa, qw, sw)
+        rows = r1
+    dt = time.perf_counter() - t0
     flops = 2.0 * rows * n * k
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {rows} of {m} token rows through the full step (weight quantisation of "
-                      f"all {n}x{k} weights, activation quantisation, fp64 GEMM); {dt:.1f} s on the host",
+            "sample": f"first {rows} of {m} token rows through the full step (weight quantisation of all "
+                      f"{n}x{k} weights once, activation quantisation, fp64 GEMM in {chunk}-row chunks until "
+                      f"{min_seconds:.0f} s had passed); {dt:.1f} s on the host",
             "seconds": round(dt, 2)}
 
 
@@ -319,9 +361,11 @@ def main():
     fp8rl.load()
     torch.cuda.init()
     if args.workload != "prefill":
-        fn = {"requant": requant, "moe": moe}.get(args.workload)
-        if fn is None:
-            raise SystemExit("decode workload: see the parity tests")
+        if args.workload == "copy":
+            print(json.dumps({"workload": "device-to-device copy of 4 GiB (torch copy_)",
+                              "GB/s": hbm_copy_reference()}), flush=True)
+            return
+        fn = {"requant": requant, "moe": moe, "decode": decode}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
     out, (a, w) = prefill(args, fp8rl)
@@ -329,7 +373,7 @@ def main():
                 "scaling": "weak", "vs_baseline": None, "data": "synthetic"})
     if not args.no_extra:
         extra = {"weight_resync": requant(args, fp8rl), "moe_grouped": moe(args, fp8rl),
-                 "hbm_copy_GB/s": hbm_copy_reference()}
+                 "decode_layer": decode(args, fp8rl), "hbm_copy_GB/s": hbm_copy_reference()}
         out["extra"] = extra
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(a, w)
