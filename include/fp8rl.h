@@ -111,6 +111,36 @@ int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64
                           void* stream);
 
 /*
+ * The same dense product (same operation and arguments as fp8rl_gemm_w8a8_block,
+ * section 2.1.1 Eq. (1) and section 2.1.4), for callers that can lend a
+ * workspace: shapes whose 128 x 128 output tiles are too few to fill the GPU
+ * (decode, m of a few hundred tokens) split the K range over several workgroups,
+ * which write fp32 partial sums to the workspace; a second kernel adds them in
+ * a fixed order and rounds to bf16 once.
+ *
+ * fp8rl_gemm_w8a8_block_workspace_size: bytes of workspace the split needs for
+ * this shape (splits * m * n * 4), 0 when the shape is not split (then
+ * fp8rl_gemm_w8a8_block_ws runs exactly fp8rl_gemm_w8a8_block) or is invalid.
+ * A pure function of (m, n, k); no device call.
+ *
+ * fp8rl_gemm_w8a8_block_ws: workspace is a DEVICE buffer of workspace_bytes,
+ * 16-byte aligned, owned by the caller, no initial contents required; it is
+ * overwritten, and two calls that overlap in time must not share it.  With
+ * workspace_bytes below the size above the call runs unsplit.  Errors: those
+ * of fp8rl_gemm_w8a8_block, then FP8RL_ERR_INVALID_ARG for workspace_bytes < 0
+ * or a NULL workspace with workspace_bytes > 0, FP8RL_ERR_MISALIGNED for a
+ * workspace not 16-byte aligned.  The split result is deterministic and meets
+ * the same tolerance; it is not bit-identical to the unsplit path (the K
+ * blocks are summed in a different fp32 order).
+ */
+int64_t fp8rl_gemm_w8a8_block_workspace_size(int64_t m, int64_t n, int64_t k);
+
+int fp8rl_gemm_w8a8_block_ws(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                             const uint8_t* qw, int64_t ldw, const float* sw,
+                             uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,
+                             void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
  * Grouped (MoE expert) blockwise-scaled FP8 GEMM (section 2.1.1: MoE expert
  * layers fc1/fc2 are quantised like every other linear layer).
  *

@@ -23,6 +23,7 @@ __all__ = [
     "LIB_PATH", "Fp8rlError", "load",
     "fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
     "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
+    "fp8rl_gemm_w8a8_block_workspace_size", "fp8rl_gemm_w8a8_block_ws",
     "fp8rl_status_string", "fp8rl_version",
     "quant_weight_block128", "quant_act_token_group128", "gemm_w8a8_block",
     "grouped_gemm_w8a8_block", "linear_w8a8",
@@ -60,11 +61,14 @@ def _load():
         "fp8rl_quant_act_token_group128": [P, I, I, I, P, I, P, I, P],
         "fp8rl_gemm_w8a8_block": [P, I, P, I, P, I, P, P, I, I, I, I, P],
         "fp8rl_grouped_gemm_w8a8_block": [P, P, I, P, P, P, I, I, P, I, I, P],
+        "fp8rl_gemm_w8a8_block_ws": [P, I, P, I, P, I, P, P, I, I, I, I, P, I, P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.fp8rl_gemm_w8a8_block_workspace_size.argtypes = [I, I, I]
+    lib.fp8rl_gemm_w8a8_block_workspace_size.restype = ctypes.c_int64
     lib.fp8rl_status_string.argtypes = [ctypes.c_int]
     lib.fp8rl_status_string.restype = ctypes.c_char_p
     lib.fp8rl_version.argtypes = []
@@ -181,10 +185,7 @@ def fp8rl_quant_act_token_group128(a: torch.Tensor, q: torch.Tensor | None = Non
     return q, scale
 
 
-def fp8rl_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
-                          y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    """y[M][N] bf16 = blockwise-scaled FP8 product of qa [M][K] (scales sa [K/128][>=M])
-    and qw [N][K] (scales sw [N/128][K/128])."""
+def _dense_args(qa, sa, qw, sw, y):
     qa, qw = _u8(qa), _u8(qw)
     m, k = qa.shape
     n, k2 = qw.shape
@@ -201,11 +202,42 @@ def fp8rl_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, 
     if y.dtype != torch.bfloat16 or tuple(y.shape) != (m, n):
         raise ValueError("y must be bf16 [M][N]")
     _dev(qa, sa, qw, sw, y)
+    return qa, qw, y, m, n, k
+
+
+def fp8rl_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
+                          y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """y[M][N] bf16 = blockwise-scaled FP8 product of qa [M][K] (scales sa [K/128][>=M])
+    and qw [N][K] (scales sw [N/128][K/128])."""
+    qa, qw, y, m, n, k = _dense_args(qa, sa, qw, sw, y)
     if m == 0:
         return y
     st = load().fp8rl_gemm_w8a8_block(qa.data_ptr(), _ld(qa), sa.data_ptr(), sa.stride(0), qw.data_ptr(),
                                    _ld(qw), sw.data_ptr(), y.data_ptr(), _ld(y), m, n, k, _stream(stream))
     _check("fp8rl_gemm_w8a8_block", st)
+    return y
+
+
+def fp8rl_gemm_w8a8_block_workspace_size(m: int, n: int, k: int) -> int:
+    """Bytes of workspace fp8rl_gemm_w8a8_block_ws splits K with for this shape (0: no split)."""
+    return int(load().fp8rl_gemm_w8a8_block_workspace_size(m, n, k))
+
+
+def fp8rl_gemm_w8a8_block_ws(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
+                             workspace: torch.Tensor, y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """fp8rl_gemm_w8a8_block with a caller-owned device workspace (any dtype, contiguous) that
+    lets shapes with too few output tiles split K; see the C header for the contract."""
+    qa, qw, y, m, n, k = _dense_args(qa, sa, qw, sw, y)
+    if not workspace.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+    _dev(qa, workspace)
+    if m == 0:
+        return y
+    nbytes = workspace.numel() * workspace.element_size()
+    st = load().fp8rl_gemm_w8a8_block_ws(qa.data_ptr(), _ld(qa), sa.data_ptr(), sa.stride(0), qw.data_ptr(),
+                                      _ld(qw), sw.data_ptr(), y.data_ptr(), _ld(y), m, n, k,
+                                      workspace.data_ptr(), nbytes, _stream(stream))
+    _check("fp8rl_gemm_w8a8_block_ws", st)
     return y
 
 

@@ -1,4 +1,5 @@
-"""Build libfp8rl.so (HIP kernels for gfx950 + the C ABI) in-tree with hipcc.
+"""Build libfp8rl.so (HIP kernels for gfx950 + the C ABI) in-tree with hipcc, and
+libfp8rl_probe.so (the MFMA-rate probe that bench.py reports next to the spec peak).
 
 Usage:  python -m paper_2601_18150_amd.build [--verbose] [--save-temps DIR]
 """
@@ -13,8 +14,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libfp8rl.so")
+PROBE_LIB = os.path.join(HERE, "libfp8rl_probe.so")
 OBJDIR = os.path.join(ROOT, "_build")
 SOURCES = ["quant.hip", "gemm.hip", "api.cpp"]
+PROBE_SOURCES = ["probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -58,14 +61,16 @@ def _compile(src, verbose=False, save_temps=None):
 def build(verbose=False, save_temps=None) -> str:
     if shutil.which(HIPCC) is None and not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
-    with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose, save_temps), SOURCES))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    srcs = SOURCES + PROBE_SOURCES
+    with concurrent.futures.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = dict(zip(srcs, ex.map(lambda s: _compile(s, verbose, save_temps), srcs)))
+    for lib, group in ((LIB, SOURCES), (PROBE_LIB, PROBE_SOURCES)):
+        tmp = lib + ".tmp"
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + [objs[s] for s in group]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, lib)
     return LIB
 
 

@@ -1,5 +1,5 @@
 // C ABI of libfp8rl (declared in include/fp8rl.h): argument validation, then
-// one launch on the caller's stream.  No allocation, no synchronisation, no
+// launches on the caller's stream.  No allocation, no synchronisation, no
 // state kept between calls.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -16,6 +16,26 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 int hip_status(hipError_t e) { return e == hipSuccess ? FP8RL_OK : FP8RL_ERR_HIP; }
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Validation shared by the dense GEMM entry points: an FP8RL_* error, FP8RL_OK for
+// a valid call with nothing to do, or kLaunch.
+constexpr int kLaunch = -1;
+
+int check_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw, int64_t ldw,
+                const float* sw, const uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k) {
+  if (m < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
+  if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m >= kMaxDim || n >= kMaxDim || k >= kMaxDim) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (((m + 127) / 128) * (n / 128) >= (int64_t(1) << 30)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m == 0 || n == 0) return FP8RL_OK;
+  if (!qa || !sa || !qw || !sw || !y) return FP8RL_ERR_INVALID_ARG;
+  if (k == 0) return FP8RL_ERR_UNSUPPORTED_SHAPE;   // an empty reduction is not a blockwise GEMM
+  if (lda < k || ldw < k || ldy < n || ld_sa < m) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(qa, 16) || !aligned(qw, 16) || !aligned(y, 16) || !aligned(sa, 4) || !aligned(sw, 4) ||
+      lda % 16 || ldw % 16 || ldy % 8)
+    return FP8RL_ERR_MISALIGNED;
+  return kLaunch;
+}
 
 }  // namespace
 
@@ -65,17 +85,30 @@ int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int6
 int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
                           int64_t ldw, const float* sw, uint16_t* y, int64_t ldy, int64_t m, int64_t n,
                           int64_t k, void* stream) {
-  if (m < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
-  if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
-  if (m >= kMaxDim || n >= kMaxDim || k >= kMaxDim) return FP8RL_ERR_UNSUPPORTED_SHAPE;
-  if (((m + 127) / 128) * (n / 128) >= (int64_t(1) << 30)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
-  if (m == 0 || n == 0) return FP8RL_OK;
-  if (!qa || !sa || !qw || !sw || !y) return FP8RL_ERR_INVALID_ARG;
-  if (k == 0) return FP8RL_ERR_UNSUPPORTED_SHAPE;   // an empty reduction is not a blockwise GEMM
-  if (lda < k || ldw < k || ldy < n || ld_sa < m) return FP8RL_ERR_INVALID_ARG;
-  if (!aligned(qa, 16) || !aligned(qw, 16) || !aligned(y, 16) || !aligned(sa, 4) || !aligned(sw, 4) ||
-      lda % 16 || ldw % 16 || ldy % 8)
-    return FP8RL_ERR_MISALIGNED;
+  const int st = check_dense(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k);
+  if (st != kLaunch) return st;
+  return hip_status(
+      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream)));
+}
+
+int64_t fp8rl_gemm_w8a8_block_workspace_size(int64_t m, int64_t n, int64_t k) {
+  if (m <= 0 || n <= 0 || k <= 0 || n % 128 || k % 128 || m >= kMaxDim || n >= kMaxDim || k >= kMaxDim) return 0;
+  const int splits = fp8rl::splitk_factor(m, n, k);
+  return splits > 1 ? int64_t(splits) * m * n * 4 : 0;
+}
+
+int fp8rl_gemm_w8a8_block_ws(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
+                             int64_t ldw, const float* sw, uint16_t* y, int64_t ldy, int64_t m, int64_t n,
+                             int64_t k, void* workspace, int64_t workspace_bytes, void* stream) {
+  const int st = check_dense(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k);
+  if (st != kLaunch) return st;
+  if (workspace_bytes < 0 || (workspace_bytes > 0 && !workspace)) return FP8RL_ERR_INVALID_ARG;
+  if (workspace_bytes > 0 && !aligned(workspace, 16)) return FP8RL_ERR_MISALIGNED;
+  const int splits = fp8rl::splitk_factor(m, n, k);
+  if (splits > 1 && workspace_bytes >= int64_t(splits) * m * n * 4)
+    return hip_status(fp8rl::launch_gemm_w8a8_block_splitk(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k,
+                                                           static_cast<float*>(workspace), splits,
+                                                           as_stream(stream)));
   return hip_status(
       fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream)));
 }

@@ -35,8 +35,7 @@ __device__ __forceinline__ int xcd_contiguous(int id, int total) {
   return x * q + min(x, r) + j;
 }
 
-__device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n) {
-  const int t = xcd_contiguous(id, tiles_m * tiles_n);
+__device__ __forceinline__ int band_tile(int t, int tiles_m, int tiles_n) {
   const int band = t / (kGroupM * tiles_n);
   const int first_m = band * kGroupM;
   const int gm = min(tiles_m - first_m, kGroupM);
@@ -44,6 +43,10 @@ __device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n
   const int tile_m = first_m + in_band % gm;
   const int tile_n = in_band / gm;
   return tile_n * tiles_m + tile_m;
+}
+
+__device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n) {
+  return band_tile(xcd_contiguous(id, tiles_m * tiles_n), tiles_m, tiles_n);
 }
 
 template <class C>
@@ -57,8 +60,60 @@ __global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_kernel(
   const int tile_n = tile / tiles_m;
   const int64_t row_lo = (int64_t)tile_m * C::BM;
   const int64_t row_hi = min(row_lo + C::BM, M);
-  gemm_tile<C>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, row_lo, row_hi, (int64_t)tile_n * C::BN, N, KB,
-               lds);
+  gemm_tile<C>(qa, lda, sa, ld_sa, qw, ldw, sw, KB, y, ldy, nullptr, 0, row_lo, row_hi, (int64_t)tile_n * C::BN,
+               N, KB, lds);
+}
+
+// Split-K dense GEMM, for shapes whose tiles alone cannot fill the GPU (decode:
+// M = 256 gives 64-96 tiles of 128x128 for the narrow layers).  Workgroup v
+// runs K range `split` of one tile and writes its fp32 sums to
+// part[split][M][N]; splitk_reduce_kernel adds the ranges in order.  Ids are
+// renumbered as in the dense kernel, split slowest, so the tiles an XCD runs
+// together share their weight rows.
+template <class C>
+__global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_splitk_kernel(
+    const uint8_t* __restrict__ qa, int64_t lda, const float* __restrict__ sa, int64_t ld_sa,
+    const uint8_t* __restrict__ qw, int64_t ldw, const float* __restrict__ sw,
+    float* __restrict__ part, int64_t M, int64_t N, int KB, int tiles_m, int tiles_n, int splits) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
+  const int total = tiles_m * tiles_n;
+  const int v = xcd_contiguous(blockIdx.x, total * splits);
+  const int split = v / total;
+  const int tile = band_tile(v - split * total, tiles_m, tiles_n);
+  const int tile_m = tile % tiles_m;
+  const int tile_n = tile / tiles_m;
+  const int kb0 = (int)(((int64_t)split * KB) / splits);
+  const int kb1 = (int)(((int64_t)(split + 1) * KB) / splits);
+  const int64_t row_lo = (int64_t)tile_m * C::BM;
+  const int64_t row_hi = min(row_lo + C::BM, M);
+  gemm_tile<C, true>(qa + (int64_t)kb0 * 128, lda, sa + (int64_t)kb0 * ld_sa, ld_sa, qw + (int64_t)kb0 * 128, ldw,
+                     sw + kb0, KB, nullptr, 0, part + (int64_t)split * M * N, N, row_lo, row_hi,
+                     (int64_t)tile_n * C::BN, N, kb1 - kb0, lds);
+}
+
+// y[m][n] = bf16_rne(part[0][m][n] + part[1][m][n] + ... ), eight n per thread.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ part, int64_t M, int64_t N,
+                                                            int splits, uint16_t* __restrict__ y, int64_t ldy) {
+  const int64_t chunks = N / 8;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= M * chunks) return;
+  const int64_t m = i / chunks;
+  const int64_t c = i - m * chunks;
+  const float* p = part + m * N + c * 8;
+  float4 a = *reinterpret_cast<const float4*>(p);
+  float4 b = *reinterpret_cast<const float4*>(p + 4);
+  for (int s = 1; s < splits; ++s) {
+    const float4 u = *reinterpret_cast<const float4*>(p + (int64_t)s * M * N);
+    const float4 w = *reinterpret_cast<const float4*>(p + (int64_t)s * M * N + 4);
+    a.x += u.x; a.y += u.y; a.z += u.z; a.w += u.w;
+    b.x += w.x; b.y += w.y; b.z += w.z; b.w += w.w;
+  }
+  uint4 o;
+  o.x = f32_to_bf16_rne(a.x) | (f32_to_bf16_rne(a.y) << 16);
+  o.y = f32_to_bf16_rne(a.z) | (f32_to_bf16_rne(a.w) << 16);
+  o.z = f32_to_bf16_rne(b.x) | (f32_to_bf16_rne(b.y) << 16);
+  o.w = f32_to_bf16_rne(b.z) | (f32_to_bf16_rne(b.w) << 16);
+  *reinterpret_cast<uint4*>(y + m * ldy + c * 8) = o;
 }
 
 // Grouped GEMM: a 1-D grid of max_tiles_m x tiles_n workgroups.  The m tile
@@ -111,8 +166,8 @@ __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
   const int KB = (int)(K / 128);
   const int64_t row_lo = (int64_t)offsets[e] + (int64_t)mt * C::BM;
   const int64_t row_hi = min(row_lo + C::BM, (int64_t)offsets[e + 1]);
-  gemm_tile<C>(qa, K, sa, ld_sa, qw + (int64_t)e * N * K, K, sw + (int64_t)e * (N / 128) * KB, y, N,
-               row_lo, row_hi, (int64_t)tile_n * C::BN, N, KB, lds);
+  gemm_tile<C>(qa, K, sa, ld_sa, qw + (int64_t)e * N * K, K, sw + (int64_t)e * (N / 128) * KB, KB, y, N,
+               nullptr, 0, row_lo, row_hi, (int64_t)tile_n * C::BN, N, KB, lds);
 }
 
 template <class C>
@@ -146,6 +201,41 @@ hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* s
   if (m >= 2048 && n >= 2048)
     return launch_dense<CfgLarge>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
   return launch_dense<CfgSmall>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+}
+
+int splitk_factor(int64_t m, int64_t n, int64_t k) {
+  // Split K only when the 128x128 tiles cover less than half of MI355X's 256
+  // CUs, into the largest power of two of ranges that keeps tiles x splits
+  // within 256, each range at least 4 K blocks long.  (Measured on the decode
+  // linears, M = 256: more ranges lose to the fp32 partial-sum traffic, which
+  // grows with the split.)
+  constexpr int64_t kCus = 256;
+  if (m <= 0 || n <= 0 || k <= 0 || (m >= 2048 && n >= 2048)) return 1;
+  const int64_t tiles = ((m + 127) / 128) * (n / 128);
+  if (2 * tiles >= kCus) return 1;
+  int64_t s = 1;
+  while (2 * s * tiles <= kCus) s *= 2;
+  const int64_t by_k = (k / 128) / 4;
+  if (s > by_k) s = by_k;
+  return s > 1 ? (int)s : 1;
+}
+
+hipError_t launch_gemm_w8a8_block_splitk(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                         const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y,
+                                         int64_t ldy, int64_t m, int64_t n, int64_t k, float* part, int splits,
+                                         hipStream_t stream) {
+  using C = CfgSmall;
+  const int tiles_m = (int)((m + C::BM - 1) / C::BM);
+  const int tiles_n = (int)(n / C::BN);
+  hipLaunchKernelGGL(gemm_w8a8_block_splitk_kernel<C>, dim3((unsigned)(tiles_m * tiles_n * splits)),
+                     dim3(C::kThreads), 0, stream, qa, lda, sa, ld_sa, qw, ldw, sw, part, m, n, (int)(k / 128),
+                     tiles_m, tiles_n, splits);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t chunks = m * (n / 8);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, stream, part, m,
+                     n, splits, y, ldy);
+  return hipGetLastError();
 }
 
 hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,

@@ -123,7 +123,10 @@ __device__ __forceinline__ void wait_vmcnt() {
 // One output tile.  Rows row_lo .. row_hi-1 of A / Y are valid for this tile
 // (row_hi - row_lo may be less than BM: loads clamp to the last valid row, stores
 // are masked).  n0 .. n0+BN-1 are the tile's weight rows; rows >= N are clamped
-// on load and masked on store.  sw points at this weight's [N/128][KB] scales.
+// on load and masked on store.  The tile sums KB K blocks starting where qa, sa,
+// qw and sw point; sw rows (one per 128 weight rows) are sw_ld floats apart.
+// kPartial: write the fp32 sums to part (row stride ldp) instead of bf16 to y
+// (one K range of a split-K product; the caller adds the ranges).
 //
 // Pipeline (STAGES-deep LDS ring, one barrier per K step):
 //   prologue: DMA K steps 0 .. STAGES-2
@@ -135,12 +138,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 // one K step; the weight scale is a wave-uniform scalar load.  The DMA is then
 // the only vector-memory traffic of the loop, so the one explicit vmcnt wait
 // per step is the only wait on global memory.
-template <class C>
+template <class C, bool kPartial = false>
 __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_t lda,
                                           const float* __restrict__ sa, int64_t ld_sa,
                                           const uint8_t* __restrict__ qw, int64_t ldw,
-                                          const float* __restrict__ sw,
+                                          const float* __restrict__ sw, int sw_ld,
                                           uint16_t* __restrict__ y, int64_t ldy,
+                                          float* __restrict__ part, int64_t ldp,
                                           int64_t row_lo, int64_t row_hi, int64_t n0, int64_t N,
                                           int KB, uint8_t* lds) {
   const int t = threadIdx.x;
@@ -175,7 +179,7 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
   //      and stores nothing)
   const bool sdma = wave < C::kScaleLoads;
   const float* sa_lane = sa + row_lo + min(wave * 64 + lane, m_valid - 1);
-  const float* swrow = sw + ((min(n0 + wn * C::WTN, N - 1) >> 7) * KB);
+  const float* swrow = sw + ((min(n0 + wn * C::WTN, N - 1) >> 7) * sw_ld);
   auto dma_stage = [&](int kb, int slot) {
     uint8_t* sbase = lds + slot * C::kStageBytes;
     const uint8_t* wb = wbase + kb * 128;
@@ -276,6 +280,21 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
 
   }
   // (the last iteration waited for every DMA: nothing is in flight here)
+
+  if constexpr (kPartial) {
+    // ---- split-K partial: the fp32 sums, four consecutive n per lane (16 bytes)
+#pragma unroll
+    for (int tn = 0; tn < C::TN; ++tn) {
+      const int nl = wn * C::WTN + tn * 16 + 4 * fg;
+#pragma unroll
+      for (int tm = 0; tm < C::TM; ++tm) {
+        const int ml = wm * C::WTM + tm * 16 + frow;
+        if (ml < m_valid && nl < n_valid)
+          *reinterpret_cast<v4f32*>(part + (row_lo + ml) * ldp + n0 + nl) = acc[tn][tm];
+      }
+    }
+    return;
+  }
 
   // ---- epilogue: fp32 -> bf16 (RNE) into a copy of the whole tile in LDS (the
   //      ring is free once every wave is past its last K step), then each

@@ -20,6 +20,15 @@ hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* s
                                   uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,
                                   hipStream_t stream);
 
+// Split-K factor the dense GEMM uses for this shape (1: no split); the
+// workspace it needs is splits * m * n fp32 values.
+int splitk_factor(int64_t m, int64_t n, int64_t k);
+
+hipError_t launch_gemm_w8a8_block_splitk(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                         const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y,
+                                         int64_t ldy, int64_t m, int64_t n, int64_t k, float* part, int splits,
+                                         hipStream_t stream);
+
 hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,
                                           const uint8_t* qw, const float* sw,
                                           const int32_t* group_offsets, int64_t num_groups,

@@ -98,6 +98,31 @@ def test_gemm_argument_errors(lib):
     assert f(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None) == OK
 
 
+def test_gemm_workspace_size(lib):
+    """The split-K workspace is a pure function of the shape: splits x M x N fp32."""
+    f = lib.fp8rl_gemm_w8a8_block_workspace_size
+    assert f(256, 4096, 12288) == 4 * 256 * 4096 * 4      # decode down: 64 tiles -> 4 splits of 24 K blocks
+    assert f(256, 6144, 4096) == 2 * 256 * 6144 * 4       # decode qkv: 96 tiles -> 2 splits
+    assert f(256, 4096, 4096) == 4 * 256 * 4096 * 4       # decode o_proj: 4 splits of 8 K blocks
+    assert f(256, 24576, 4096) == 0                       # 384 tiles fill the GPU
+    assert f(8192, 24576, 4096) == 0                      # 256x256 tiles, never split
+    assert f(64, 512, 512) == 0                           # 4 K blocks: no split shorter than 4
+    assert f(37, 384, 13 * 128) == 3 * 37 * 384 * 4       # uneven split of 13 K blocks
+    for bad in [(0, 128, 128), (8, 200, 128), (8, 128, 192), (-1, 128, 128), (8, 128, 0)]:
+        assert f(*bad) == 0
+
+
+def test_gemm_ws_argument_errors(lib):
+    f = lib.fp8rl_gemm_w8a8_block_ws
+    #      qa  lda  sa  ld_sa qw  ldw  sw  y   ldy  m  n    k    ws   ws_bytes
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 200, 8, 200, 128, A16, 1 << 20, None) == SHAPE
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, A16, -1, None) == INVALID
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None, 64, None) == INVALID
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, A16 + 4, 64, None) == MISALIGNED
+    assert f(A16 + 8, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, A16, 64, None) == MISALIGNED
+    assert f(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None, 0, None) == OK
+
+
 def test_grouped_gemm_argument_errors(lib):
     f = lib.fp8rl_grouped_gemm_w8a8_block
     #        qa  sa  ld_sa qw  sw  off  G  R   y   n    k

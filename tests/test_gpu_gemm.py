@@ -204,6 +204,55 @@ def test_gemm_decode_layer(fp8rl):
         check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), name)
 
 
+def run_dense_ws(fp8rl, qa, sa, qw, sw, ws_bytes=None):
+    """The split-K entry point with the workspace it asks for (or ws_bytes)."""
+    m, k = qa.shape
+    n = qw.shape[0]
+    need = fp8rl.fp8rl_gemm_w8a8_block_workspace_size(m, n, k)
+    nbytes = need if ws_bytes is None else ws_bytes
+    ws = torch.full((max(nbytes, 16) // 4,), float("nan"), dtype=torch.float32, device="cuda")
+    y = fp8rl.fp8rl_gemm_w8a8_block_ws(to_dev(qa), to_dev(sa), to_dev(qw), to_dev(sw), ws[: nbytes // 4])
+    torch.cuda.synchronize()
+    return y, need
+
+
+def test_gemm_split_k_decode_layer(fp8rl):
+    """The four decode linears through the split-K entry point (workspace pre-filled with NaN:
+    every partial the reduction reads must have been written)."""
+    acts = synth.decode_activations()
+    ws = synth.layer_weights(35)
+    for name, (k, n) in synth.QWEN3_8B_LINEARS.items():
+        announce(f"gemm split-K decode M=256 {name} {k}->{n}")
+        x = acts["inter"] if k == 12288 else acts["h"]
+        qa, sa = cref.quant_act_token_group128(u16(x))
+        qw, sw = cref.quant_weight_block128(u16(ws[name]))
+        y, need = run_dense_ws(fp8rl, qa, sa, qw, sw)
+        assert (need > 0) == (name != "gate_up"), (name, need)
+        check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"split-K {name}")
+
+
+@pytest.mark.parametrize("m,n,k", [(1, 128, 1024), (37, 384, 13 * 128), (100, 256, 2048), (255, 640, 1024)])
+def test_gemm_split_k_ragged(fp8rl, m, n, k):
+    """Ragged M and N tails and a K range that does not divide evenly among the splits."""
+    announce(f"gemm split-K m={m} n={n} k={k}")
+    qa, sa, qw, sw = quantised_operands(m, n, k, m * 11 + n + k)
+    y, need = run_dense_ws(fp8rl, qa, sa, qw, sw)
+    assert need > 0
+    check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"split-K {m}x{n}x{k}")
+    y2, _ = run_dense_ws(fp8rl, qa, sa, qw, sw)
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16)), "split-K result not deterministic"
+
+
+def test_gemm_split_k_short_workspace_runs_unsplit(fp8rl):
+    """Less workspace than the query asks for: exactly the unsplit kernel's bits."""
+    announce("gemm split-K with a short workspace")
+    qa, sa, qw, sw = quantised_operands(100, 256, 2048, 5)
+    y_ws, need = run_dense_ws(fp8rl, qa, sa, qw, sw, ws_bytes=1024)
+    assert need > 1024
+    y = run_dense(fp8rl, qa, sa, qw, sw)
+    assert torch.equal(y_ws.view(torch.int16), y.view(torch.int16))
+
+
 def test_gemm_prefill_full_size_sampled_rows(fp8rl):
     """8192x4096 -> 24576 with outliers: the full GEMM on the GPU, the oracle on sampled rows."""
     announce("gemm prefill 8192x4096x24576")
