@@ -157,7 +157,8 @@ int fp8rl_gemm_w8a8_block_ws(const uint8_t* qa, int64_t lda, const float* sa, in
  *               offsets[num_groups] == total_rows (precondition, not checked:
  *               checking would need a device read)
  * y             [total_rows][n] bf16 out, contiguous
- * n, k multiples of 128; num_groups >= 1; total_rows >= 0 (0 is a no-op).
+ * n, k multiples of 128; 1 <= num_groups <= 1024 (more: FP8RL_ERR_UNSUPPORTED_SHAPE);
+ * total_rows >= 0 (0 is a no-op).
  * Alignment: qa, qw, y 16-byte aligned; k % 16 == 0 follows from k % 128 == 0.
  */
 int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,

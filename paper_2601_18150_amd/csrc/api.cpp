@@ -119,7 +119,7 @@ int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld
   if (total_rows < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
   if (num_groups < 1) return FP8RL_ERR_INVALID_ARG;
   if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
-  if (total_rows >= kMaxDim || n >= kMaxDim || k >= kMaxDim || num_groups >= (int64_t(1) << 20) ||
+  if (total_rows >= kMaxDim || n >= kMaxDim || k >= kMaxDim || num_groups > 1024 ||
       (total_rows / 128 + num_groups) * (n / 128) >= (int64_t(1) << 31))
     return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (total_rows == 0 || n == 0) return FP8RL_OK;

@@ -49,19 +49,55 @@ __device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n
   return band_tile(xcd_contiguous(id, tiles_m * tiles_n), tiles_m, tiles_n);
 }
 
+// The cross-tile pipeline (next tile's first load during this tile's last
+// step) for the 128x128 tiles; the 256x256 tile has no registers to spare for
+// the next tile's load plan and runs one tile per workgroup.
+template <class C>
+constexpr bool kCrossTiles = C::BN * C::BM <= 128 * 128;
+
+// Job providers for gemm_tiles (see gemm_core.hpp): wave-uniform, no LDS
+// writes, no synchronisation.
+
+// Dense: a persistent grid; workgroup b runs tiles v = b, b + gridDim.x, ... of
+// the renumbered order above (with gridDim.x a multiple of 8 every tile a
+// workgroup runs is in its own XCD's range).
+template <class C>
+struct DenseJobs {
+  int v, stride, tiles_m, tiles_n, M;
+  __device__ bool next(TileJob& j) {
+    if (v >= tiles_m * tiles_n) return false;
+    const int tile = xcd_grouped_tile(v, tiles_m, tiles_n);
+    v += stride;
+    const int tile_m = tile % tiles_m;
+    j.row_lo = tile_m * C::BM;
+    j.m_valid = min(C::BM, M - j.row_lo);
+    j.n0 = (tile / tiles_m) * C::BN;
+    j.qw_off = 0;
+    j.sw_off = 0;
+    return true;
+  }
+};
+
+// A single given tile.
+struct OneJob {
+  TileJob job;
+  bool done;
+  __device__ bool next(TileJob& j) {
+    if (done) return false;
+    j = job;
+    done = true;
+    return true;
+  }
+};
+
 template <class C>
 __global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_kernel(
     const uint8_t* __restrict__ qa, int64_t lda, const float* __restrict__ sa, int64_t ld_sa,
     const uint8_t* __restrict__ qw, int64_t ldw, const float* __restrict__ sw,
-    uint16_t* __restrict__ y, int64_t ldy, int64_t M, int64_t N, int KB, int tiles_m) {
+    uint16_t* __restrict__ y, int64_t ldy, int64_t M, int64_t N, int KB, int tiles_m, int tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
-  const int tile = xcd_grouped_tile(blockIdx.x, tiles_m, (int)gridDim.x / tiles_m);
-  const int tile_m = tile % tiles_m;
-  const int tile_n = tile / tiles_m;
-  const int64_t row_lo = (int64_t)tile_m * C::BM;
-  const int64_t row_hi = min(row_lo + C::BM, M);
-  gemm_tile<C>(qa, lda, sa, ld_sa, qw, ldw, sw, KB, y, ldy, nullptr, 0, row_lo, row_hi, (int64_t)tile_n * C::BN,
-               N, KB, lds);
+  DenseJobs<C> jobs{(int)blockIdx.x, (int)gridDim.x, tiles_m, tiles_n, (int)M};
+  gemm_tiles<C, false, kCrossTiles<C>>(qa, lda, sa, ld_sa, qw, ldw, sw, KB, y, ldy, nullptr, (int)N, KB, jobs, lds);
 }
 
 // Split-K dense GEMM, for shapes whose tiles alone cannot fill the GPU (decode:
@@ -81,14 +117,17 @@ __global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_splitk_kernel(
   const int split = v / total;
   const int tile = band_tile(v - split * total, tiles_m, tiles_n);
   const int tile_m = tile % tiles_m;
-  const int tile_n = tile / tiles_m;
   const int kb0 = (int)(((int64_t)split * KB) / splits);
   const int kb1 = (int)(((int64_t)(split + 1) * KB) / splits);
-  const int64_t row_lo = (int64_t)tile_m * C::BM;
-  const int64_t row_hi = min(row_lo + C::BM, M);
-  gemm_tile<C, true>(qa + (int64_t)kb0 * 128, lda, sa + (int64_t)kb0 * ld_sa, ld_sa, qw + (int64_t)kb0 * 128, ldw,
-                     sw + kb0, KB, nullptr, 0, part + (int64_t)split * M * N, N, row_lo, row_hi,
-                     (int64_t)tile_n * C::BN, N, kb1 - kb0, lds);
+  OneJob jobs;
+  jobs.done = false;
+  jobs.job.row_lo = tile_m * C::BM;
+  jobs.job.m_valid = (int)min((int64_t)C::BM, M - jobs.job.row_lo);
+  jobs.job.n0 = (tile / tiles_m) * C::BN;
+  jobs.job.qw_off = (int64_t)kb0 * 128;
+  jobs.job.sw_off = kb0;
+  gemm_tiles<C, true, false>(qa + (int64_t)kb0 * 128, lda, sa + (int64_t)kb0 * ld_sa, ld_sa, qw, ldw, sw, KB, nullptr, 0,
+                      part + (int64_t)split * M * N, (int)N, kb1 - kb0, jobs, lds);
 }
 
 // y[m][n] = bf16_rne(part[0][m][n] + part[1][m][n] + ... ), eight n per thread.
@@ -116,59 +155,93 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   *reinterpret_cast<uint4*>(y + m * ldy + c * 8) = o;
 }
 
-// Grouped GEMM: a 1-D grid of max_tiles_m x tiles_n workgroups.  The m tile
-// index counts over all experts in order (expert e owns ceil(rows_e / BM)
-// consecutive m tiles); the grid is sized for the worst case
-// (total_rows / BM + num_groups) and workgroups past the last real tile exit at
-// once.  Ids are renumbered so that each XCD walks a contiguous range, m tile
-// fastest: the m tiles of one expert that share a weight slab run on the same
-// XCD and read it from its L2.
+// Grouped GEMM: m tiles are numbered over all experts in order (expert e owns
+// ceil(rows_e / BM) consecutive m tiles, empty experts none).  Each workgroup
+// first builds, in LDS, the first m tile and the first row of every expert
+// from the device offsets (one prefix scan by wave 0), then runs tiles
+// v = b, b + gridDim.x, ... of the (m tile, n tile) grid, renumbered so that
+// each XCD walks a contiguous range with the m tile fastest: the m tiles of one
+// expert that share a weight slab run on the same XCD and read it from its L2.
+constexpr int kMaxExperts = 1024;          // table capacity (LDS: 8 KiB)
+
+template <class C>
+struct GroupedJobs {
+  int v, stride, real_m, tiles_n, G;
+  const int* tstart;                       // LDS [G+1]: first m tile of expert e
+  const int* rstart;                       // LDS [G+1]: first row of expert e
+  int64_t N, K;
+  __device__ bool next(TileJob& j) {
+    if (v >= real_m * tiles_n) return false;
+    const int lin = xcd_contiguous(v, real_m * tiles_n);
+    v += stride;
+    const int target = lin % real_m;
+    const int tile_n = lin / real_m;
+    // e = (number of experts whose first m tile is <= target) - 1: the last
+    // such expert owns the tile (empty experts share their start with the next)
+    const int lane = threadIdx.x & 63;
+    int cnt = 0;
+    for (int e0 = 0; e0 <= G; e0 += 64) {
+      const int e = e0 + lane;
+      const bool le = e <= G && tstart[e] <= target;
+      const unsigned long long mask = __ballot(le);
+      cnt += __popcll(mask);
+      if (~mask) break;
+    }
+    // (the table entries are wave-uniform: keep them in scalar registers)
+    const int e = __builtin_amdgcn_readfirstlane(cnt - 1);
+    const int mt = target - __builtin_amdgcn_readfirstlane(tstart[e]);
+    j.row_lo = __builtin_amdgcn_readfirstlane(rstart[e]) + mt * C::BM;
+    j.m_valid = min(C::BM, __builtin_amdgcn_readfirstlane(rstart[e + 1]) - j.row_lo);
+    j.n0 = tile_n * C::BN;
+    j.qw_off = (int64_t)e * N * K;
+    j.sw_off = (int64_t)e * (N / 128) * (K / 128);
+    return true;
+  }
+};
+
 template <class C>
 __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
     const uint8_t* __restrict__ qa, const float* __restrict__ sa, int64_t ld_sa,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw,
-    const int32_t* __restrict__ offsets, int G, uint16_t* __restrict__ y, int64_t N, int64_t K,
-    int max_tiles_m) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
-  __shared__ int found[2];
+    const int32_t* __restrict__ offsets, int G, uint16_t* __restrict__ y, int64_t N, int64_t K, int tiles_n) {
+  // one LDS object: the ring, then the two expert tables
+  __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes + 2 * 4 * (kMaxExperts + 1)];
+  int* tstart = reinterpret_cast<int*>(lds + C::kLdsBytes);
+  int* rstart = tstart + (kMaxExperts + 1);
   const int t = threadIdx.x;
-  const int lin = xcd_contiguous(blockIdx.x, (int)gridDim.x);
-  const int target = lin % max_tiles_m;
-  const int tile_n = lin / max_tiles_m;
-  if (t == 0) found[0] = -1;
-  __syncthreads();
   if (t < 64) {
-    // wave 0 scans the experts 64 at a time: inclusive prefix sum of tile counts
+    // wave 0: exclusive prefix sum of the experts' m-tile counts, 64 at a time
     int base = 0;
-    for (int e0 = 0; e0 < G; e0 += 64) {
+    for (int e0 = 0; e0 <= G; e0 += 64) {
       const int e = e0 + t;
-      int cnt = 0;
-      if (e < G) cnt = (offsets[e + 1] - offsets[e] + C::BM - 1) / C::BM;
+      int cnt = 0, r0 = 0;
+      if (e <= G) r0 = offsets[e];
+      if (e < G) cnt = (offsets[e + 1] - r0 + C::BM - 1) / C::BM;
       int incl = cnt;
 #pragma unroll
       for (int d = 1; d < 64; d <<= 1) {
-        const int v = __shfl_up(incl, d, 64);
-        if (t >= d) incl += v;
+        const int u = __shfl_up(incl, d, 64);
+        if (t >= d) incl += u;
       }
-      const int excl = incl - cnt;
-      if (cnt > 0 && target >= base + excl && target < base + incl) {
-        found[0] = e;
-        found[1] = target - base - excl;
+      if (e <= G) {
+        tstart[e] = base + incl - cnt;
+        rstart[e] = r0;
       }
       base += __shfl(incl, 63, 64);
-      if (target < base) break;
     }
   }
   __syncthreads();
-  const int e = found[0];
-  if (e < 0) return;                       // uniform: past the last real tile
-  const int mt = found[1];
+  GroupedJobs<C> jobs{(int)blockIdx.x, (int)gridDim.x, __builtin_amdgcn_readfirstlane(tstart[G]), tiles_n, G,
+                      tstart, rstart, N, K};
   const int KB = (int)(K / 128);
-  const int64_t row_lo = (int64_t)offsets[e] + (int64_t)mt * C::BM;
-  const int64_t row_hi = min(row_lo + C::BM, (int64_t)offsets[e + 1]);
-  gemm_tile<C>(qa, K, sa, ld_sa, qw + (int64_t)e * N * K, K, sw + (int64_t)e * (N / 128) * KB, KB, y, N,
-               nullptr, 0, row_lo, row_hi, (int64_t)tile_n * C::BN, N, KB, lds);
+  gemm_tiles<C, false, kCrossTiles<C>>(qa, K, sa, ld_sa, qw, K, sw, KB, y, N, nullptr, (int)N, KB, jobs, lds);
 }
+
+// Workgroups that stay resident on one CU for a configuration (LDS-limited).
+template <class C, int kExtraLds = 0>
+constexpr int per_cu() { return (160 * 1024) / (C::kLdsBytes + kExtraLds); }
+
+constexpr int kCus = 256;     // MI355X; grids of kCus * per_cu() are multiples of 8 (one per XCD)
 
 template <class C>
 hipError_t launch_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
@@ -176,8 +249,13 @@ hipError_t launch_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t
                         int64_t k, hipStream_t stream) {
   const int tiles_m = (int)((m + C::BM - 1) / C::BM);
   const int tiles_n = (int)((n + C::BN - 1) / C::BN);
-  hipLaunchKernelGGL(gemm_w8a8_block_kernel<C>, dim3((unsigned)(tiles_m * tiles_n)), dim3(C::kThreads), 0,
-                     stream, qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, (int)(k / 128), tiles_m);
+  const int64_t total = (int64_t)tiles_m * tiles_n;
+  // persistent grid with the cross-tile pipeline, else one workgroup per tile
+  // (a persistent grid without it measured no faster)
+  const int64_t slots = kCrossTiles<C> ? (int64_t)kCus * per_cu<C>() : total;
+  hipLaunchKernelGGL(gemm_w8a8_block_kernel<C>, dim3((unsigned)(total < slots ? total : slots)),
+                     dim3(C::kThreads), 0, stream, qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n,
+                     (int)(k / 128), tiles_m, tiles_n);
   return hipGetLastError();
 }
 
@@ -185,11 +263,13 @@ template <class C>
 hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw,
                           const float* sw, const int32_t* offsets, int64_t g, int64_t rows, uint16_t* y,
                           int64_t n, int64_t k, hipStream_t stream) {
-  const int64_t max_tiles_m = rows / C::BM + g;
+  const int64_t max_tiles_m = rows / C::BM + g;        // upper bound on the real m tiles
   const int64_t tiles_n = (n + C::BN - 1) / C::BN;
-  hipLaunchKernelGGL(grouped_gemm_w8a8_block_kernel<C>, dim3((unsigned)(max_tiles_m * tiles_n)),
+  const int64_t total = max_tiles_m * tiles_n;
+  const int64_t slots = (int64_t)kCus * per_cu<C, 2 * 4 * (kMaxExperts + 1)>();
+  hipLaunchKernelGGL(grouped_gemm_w8a8_block_kernel<C>, dim3((unsigned)(total < slots ? total : slots)),
                      dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw, sw, offsets, (int)g, y, n, k,
-                     (int)max_tiles_m);
+                     (int)tiles_n);
   return hipGetLastError();
 }
 

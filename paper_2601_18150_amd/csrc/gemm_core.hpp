@@ -113,6 +113,18 @@ __device__ __forceinline__ void store_stream16(uint16_t* p, const uint4& v) {
   __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t*>(p));
 }
 
+// Workgroup barrier for data shared through LDS only: waits for this wave's
+// LDS operations (lgkmcnt(0)), then s_barrier.  Unlike __syncthreads() it does
+// not wait for outstanding global stores or DMA loads (their vmcnt waits are
+// explicit); the empty asm statements keep the compiler from moving memory
+// operations across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x3 << 14));   // lgkmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // s_waitcnt vmcnt(n) only (expcnt and lgkmcnt left at their maxima)
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -120,84 +132,58 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// One output tile.  Rows row_lo .. row_hi-1 of A / Y are valid for this tile
-// (row_hi - row_lo may be less than BM: loads clamp to the last valid row, stores
-// are masked).  n0 .. n0+BN-1 are the tile's weight rows; rows >= N are clamped
-// on load and masked on store.  The tile sums KB K blocks starting where qa, sa,
-// qw and sw point; sw rows (one per 128 weight rows) are sw_ld floats apart.
-// kPartial: write the fp32 sums to part (row stride ldp) instead of bf16 to y
-// (one K range of a split-K product; the caller adds the ranges).
+// One output tile to compute (wave-uniform values, produced by a job provider).
+struct TileJob {
+  int row_lo;              // first row of A / Y
+  int m_valid;             // rows of the tile that exist, 1 .. BM
+  int n0;                  // first weight row (output column)
+  int64_t qw_off;          // weight codes of this tile's matrix: qw + qw_off, [N][ldw]
+  int64_t sw_off;          // its block scales: sw + sw_off, rows of sw_ld floats
+  // (offsets rather than pointers: addresses derived from the kernel's
+  // __restrict__ arguments keep their no-alias, read-only provenance, so the
+  // compiler neither orders the output stores after the operand loads nor turns
+  // the scale reads into vector loads)
+};
+
+// Tiles of  Y^T = W . A^T  computed by one workgroup, one after another; the
+// job provider `jobs` hands them out (jobs.next(j) returns false at the end; it
+// must not touch LDS or synchronise).  Rows >= M of a tile are clamped on load
+// and masked on store, weight rows >= N likewise.  Each tile sums KB K blocks
+// starting where qa, sa, qw + qw_off and sw + sw_off point; sw rows (one per
+// 128 weight rows) are sw_ld floats apart.  kPartial: write the fp32 sums to part (rows of
+// N floats) instead of bf16 to y (one K range of a split-K product).
 //
-// Pipeline (STAGES-deep LDS ring, one barrier per K step):
-//   prologue: DMA K steps 0 .. STAGES-2
-//   step kb:  wait for this wave's DMA of step kb; barrier (all waves' DMA of
-//             step kb landed, all waves done reading step kb-1's slot);
-//             MFMA + scale-FMA on slot kb % STAGES, with the DMA of step
-//             kb+STAGES-1 into the slot freed by step kb-1 interleaved.
+// Pipeline (2-slot LDS ring, one barrier per K step):
+//   step s:  wait for this wave's DMA of step s; barrier (all waves' DMA of step
+//            s landed, all waves done reading step s-1's slot); MFMA + scale-FMA
+//            on slot s % 2, with the DMA of step s+1 into the other slot
+//            interleaved.
+//   kCross:  after a tile's last K block, step s+1 is the first K block of the
+//            workgroup's next tile, so consecutive tiles form one pipeline and
+//            the next tile's first load overlaps this tile's last step and
+//            output.  Without it the workgroup computes its first tile only
+//            (the 256x256 tile, whose registers are full, runs one tile per
+//            workgroup).
+//   tile end: the bf16 tile is staged through the slot of its last step (in
+//            row groups that fit one slot) and written as whole output rows.
 // A slot holds the W tile, the A tile and the tile's BM activation scales of
 // one K step; the weight scale is a wave-uniform scalar load.  The DMA is then
 // the only vector-memory traffic of the loop, so the one explicit vmcnt wait
-// per step is the only wait on global memory.
-template <class C, bool kPartial = false>
-__device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_t lda,
-                                          const float* __restrict__ sa, int64_t ld_sa,
-                                          const uint8_t* __restrict__ qw, int64_t ldw,
-                                          const float* __restrict__ sw, int sw_ld,
-                                          uint16_t* __restrict__ y, int64_t ldy,
-                                          float* __restrict__ part, int64_t ldp,
-                                          int64_t row_lo, int64_t row_hi, int64_t n0, int64_t N,
-                                          int KB, uint8_t* lds) {
+// per step is the only wait on global memory (at a tile's first step it also
+// covers the previous tile's output stores).
+template <class C, bool kPartial, bool kCross, class Jobs>
+__device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64_t lda,
+                                           const float* __restrict__ sa, int64_t ld_sa,
+                                           const uint8_t* __restrict__ qw, int64_t ldw,
+                                           const float* __restrict__ sw, int sw_ld,
+                                           uint16_t* __restrict__ y, int64_t ldy, float* __restrict__ part,
+                                           int N, int KB, Jobs& jobs, uint8_t* lds) {
+  static_assert(C::STAGES == 2, "the tile pipeline is written for a 2-slot ring");
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wn = wave % C::WN;
   const int wm = wave / C::WN;
-  const int n_valid = (int)min((int64_t)C::BN, N - n0);        // >= 1
-  const int m_valid = (int)(row_hi - row_lo);                  // >= 1
-
-  // ---- DMA plan: wave w moves row octets w, w + kWaves, ...  In an octet,
-  //      lane L lands at row 8o + (L >> 3), physical chunk (L & 7), which holds
-  //      logical chunk (L & 7) ^ swz_key(row) of the swizzled layout.
-  const int lrow = lane >> 3;
-  uint32_t goff[C::kLoadsPerWave];
-  bool is_w[C::kLoadsPerWave];
-#pragma unroll
-  for (int i = 0; i < C::kLoadsPerWave; ++i) {
-    const int o = wave + i * C::kWaves;                 // wave-uniform
-    is_w[i] = o < C::BN / 8;
-    const int r = (is_w[i] ? o : o - C::BN / 8) * 8 + lrow;
-    const int lchunk = (lane & 7) ^ swz_key(r);
-    goff[i] = is_w[i] ? (uint32_t)(min(r, n_valid - 1) * ldw + lchunk * 16)
-                      : (uint32_t)(min(r, m_valid - 1) * lda + lchunk * 16);
-  }
-  const uint8_t* wbase = qw + n0 * ldw;
-  const uint8_t* abase = qa + row_lo * lda;
-
-  // ---- scales: wave w < kScaleLoads DMAs tokens 64w .. 64w+63 of the tile
-  //      (clamped to the last valid row); this wave's 128-row weight scale
-  //      block is read with scalar loads (a wave past N reads the last block
-  //      and stores nothing)
-  const bool sdma = wave < C::kScaleLoads;
-  const float* sa_lane = sa + row_lo + min(wave * 64 + lane, m_valid - 1);
-  const float* swrow = sw + ((min(n0 + wn * C::WTN, N - 1) >> 7) * sw_ld);
-  auto dma_stage = [&](int kb, int slot) {
-    uint8_t* sbase = lds + slot * C::kStageBytes;
-    const uint8_t* wb = wbase + kb * 128;
-    const uint8_t* ab = abase + kb * 128;
-#pragma unroll
-    for (int i = 0; i < C::kLoadsPerWave; ++i) {
-      const int o = wave + i * C::kWaves;
-      lds_dma16((is_w[i] ? wb : ab) + goff[i], sbase + o * 1024);
-    }
-    if (sdma) lds_dma4(sa_lane + (int64_t)kb * ld_sa, sbase + C::kWBytes + C::kABytes + wave * 256);
-  };
-
-  v4f32 acc[C::TN][C::TM];
-#pragma unroll
-  for (int i = 0; i < C::TN; ++i)
-#pragma unroll
-    for (int j = 0; j < C::TM; ++j) acc[i][j] = (v4f32){0.f, 0.f, 0.f, 0.f};
-
   const int frow = lane & 15;
   const int fg = lane >> 4;
   // fragment byte offsets inside a tile: row frow (+16 per sub-tile), chunks 2g, 2g+1
@@ -205,131 +191,211 @@ __device__ __forceinline__ void gemm_tile(const uint8_t* __restrict__ qa, int64_
   const int f0 = swz(frow, 2 * fg);
   const int f1 = swz(frow, 2 * fg + 1);
 
-  // prologue
+  // ---- DMA plan: wave w moves row octets w, w + kWaves, ...  In an octet,
+  //      lane L lands at row 8o + (L >> 3), physical chunk (L & 7), which holds
+  //      logical chunk (L & 7) ^ swz_key(row) of the swizzled layout.  The
+  //      per-lane byte offsets clamp rows past the tile's valid range.
+  const int lrow = lane >> 3;
+  auto dma_offsets = [&](uint32_t (&g)[C::kLoadsPerWave], int n_valid, int m_valid) {
 #pragma unroll
-  for (int s = 0; s < C::STAGES - 1; ++s)
-    if (s < KB) dma_stage(s, s);
-
-  for (int kb = 0; kb < KB; ++kb) {
-    // step kb's DMA is the oldest still outstanding: up to STAGES-2 younger
-    // stages (kLoadsPerWave tile loads + at most one scale load each) may stay
-    // in flight; near the end of K fewer were issued, so wait for everything
-    if (kb + C::STAGES - 2 < KB) {
-      if (sdma)
-        wait_vmcnt<(C::STAGES - 2) * (C::kLoadsPerWave + 1)>();
-      else
-        wait_vmcnt<(C::STAGES - 2) * C::kLoadsPerWave>();
-    } else {
-      wait_vmcnt<0>();
+    for (int i = 0; i < C::kLoadsPerWave; ++i) {
+      const int o = wave + i * C::kWaves;               // wave-uniform
+      const bool w = o < C::BN / 8;
+      const int r = (w ? o : o - C::BN / 8) * 8 + lrow;
+      const int lchunk = (lane & 7) ^ swz_key(r);
+      g[i] = w ? (uint32_t)(min(r, n_valid - 1) * ldw + lchunk * 16)
+               : (uint32_t)(min(r, m_valid - 1) * lda + lchunk * 16);
     }
-    __syncthreads();
+  };
+  // scales: wave w < kScaleLoads DMAs tokens 64w .. 64w+63 of the tile (clamped
+  // to the last valid row); this wave's 128-row weight scale block is read with
+  // scalar loads (a wave past N reads the last block and stores nothing)
+  const bool sdma = wave < C::kScaleLoads;
+  auto n_valid_of = [&](const TileJob& j) { return min(C::BN, N - j.n0); };
+  auto sa_lane_of = [&](const TileJob& j) { return sa + j.row_lo + min(wave * 64 + lane, j.m_valid - 1); };
 
-    // refill the slot released by step kb-1 with step kb+STAGES-1 (none past
-    // the end of K).  With 8 sub-tile rows per wave the DMA instructions are
-    // spread over the first half of the sub-tile loop below (issued all at once
-    // they stall the wave on a full address queue, issued later they arrive
-    // after the next barrier); with fewer, all are issued with the first one
-    // (measured fastest for the 128x128 tiles).
-    const bool refill = kb + C::STAGES - 1 < KB;
-    const int kd = min(kb + C::STAGES - 1, KB - 1);   // (only used when refill)
-    uint8_t* dslot = lds + ((kb + C::STAGES - 1) % C::STAGES) * C::kStageBytes;
-    const uint8_t* dwb = wbase + kd * 128;
-    const uint8_t* dab = abase + kd * 128;
+  TileJob cur;
+  if (!jobs.next(cur)) return;
+  TileJob nxt = cur;
+  bool has_nxt = false;
+  uint32_t goff[C::kLoadsPerWave], goff_n[C::kLoadsPerWave];
+  dma_offsets(goff, n_valid_of(cur), cur.m_valid);
+  if constexpr (kCross) {
+    has_nxt = jobs.next(nxt);
+    if (has_nxt) dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid);
+  }
 
-    constexpr int kDmaSpread = C::TN >= 8 ? C::TN / 2 : 1;   // sub-tile rows that carry DMA issue
-    const uint8_t* st = lds + (kb % C::STAGES) * C::kStageBytes;
-    const float* sts = reinterpret_cast<const float*>(st + C::kWBytes + C::kABytes) + wm * C::WTM + (lane & 15);
-    const float swv = swrow[kb];
-    float sc[C::TM];
+  // prologue: the first tile's first K block into slot 0
+  {
+    const uint8_t* wb = qw + cur.qw_off + (int64_t)cur.n0 * ldw;
+    const uint8_t* ab = qa + (int64_t)cur.row_lo * lda;
 #pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sts[tm * 16] * swv;
+    for (int i = 0; i < C::kLoadsPerWave; ++i) {
+      const int o = wave + i * C::kWaves;
+      lds_dma16((o < C::BN / 8 ? wb : ab) + goff[i], lds + o * 1024);
+    }
+    if (sdma) lds_dma4(sa_lane_of(cur), lds + C::kWBytes + C::kABytes + wave * 256);
+  }
 
-    const uint8_t* sta = st + C::kWBytes + wm * C::WTM * 128;
-    const uint8_t* stw = st + wn * C::WTN * 128;
-    // first weight fragment, then the activation fragments in the order the
-    // first MFMAs consume them (LDS returns in order, so each MFMA waits only
-    // for its own operands); weight fragments are double-buffered: the next
-    // sub-tile's read is in flight while this one's MFMAs run
-    v8i32 af = lds_frag2(stw, f0, f1);
-    v8i32 bf[C::TM];
+  int slot = 0;
+  for (;;) {
+    const int n_valid = n_valid_of(cur);
+    const uint8_t* wbase = qw + cur.qw_off + (int64_t)cur.n0 * ldw;
+    const uint8_t* abase = qa + (int64_t)cur.row_lo * lda;
+    const float* sa_lane = sa_lane_of(cur);
+    const float* swrow = sw + cur.sw_off + (int64_t)(min(cur.n0 + wn * C::WTN, N - 1) >> 7) * sw_ld;
+
+    v4f32 acc[C::TN][C::TM];
 #pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm) bf[tm] = lds_frag2(sta + tm * 16 * 128, f0, f1);
+    for (int i = 0; i < C::TN; ++i)
 #pragma unroll
-    for (int tn = 0; tn < C::TN; ++tn) {
-#pragma unroll
-      for (int i = 0; i < C::kLoadsPerWave; ++i) {
-        if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill) {
-          const int o = wave + i * C::kWaves;
-          lds_dma16((is_w[i] ? dwb : dab) + goff[i], dslot + o * 1024);
+      for (int j = 0; j < C::TM; ++j) acc[i][j] = (v4f32){0.f, 0.f, 0.f, 0.f};
+
+    for (int kb = 0; kb < KB; ++kb) {
+      wait_vmcnt<0>();        // this step's DMA (and a previous tile's output stores)
+      lds_barrier();
+
+      // refill the other slot with the next step: the next K block of this tile
+      // or, after its last, the first K block of the next tile (if any).  With 8
+      // sub-tile rows per wave the DMA instructions are spread over the first
+      // half of the sub-tile loop below (issued all at once they stall the wave
+      // on a full address queue, issued later they arrive after the next
+      // barrier); with fewer, all are issued with the first one (measured
+      // fastest for the 128x128 tiles).
+      const bool last = kb + 1 == KB;
+      const bool refill = !last || has_nxt;
+      uint8_t* dslot = lds + (slot ^ 1) * C::kStageBytes;
+      const uint8_t* dwb = wbase + (kb + 1) * 128;
+      const uint8_t* dab = abase + (kb + 1) * 128;
+      const float* dsa = sa_lane + (int64_t)(kb + 1) * ld_sa;
+      if constexpr (kCross) {
+        if (last) {
+          dwb = qw + nxt.qw_off + (int64_t)nxt.n0 * ldw;
+          dab = qa + (int64_t)nxt.row_lo * lda;
+          dsa = sa_lane_of(nxt);
         }
       }
-      if (tn == 0 && sdma && refill) lds_dma4(sa_lane + (int64_t)kd * ld_sa, dslot + C::kWBytes + C::kABytes + wave * 256);
-      v8i32 af_next = af;
-      if (tn + 1 < C::TN) af_next = lds_frag2(stw + (tn + 1) * 16 * 128, f0, f1);
-      // all MFMAs of the sub-tile row first (independent results in flight),
-      // then their scale FMAs
-      v4f32 p[C::TM];
+
+      constexpr int kDmaSpread = C::TN >= 8 ? C::TN / 2 : 1;   // sub-tile rows that carry DMA issue
+      const uint8_t* st = lds + slot * C::kStageBytes;
+      const float* sts = reinterpret_cast<const float*>(st + C::kWBytes + C::kABytes) + wm * C::WTM + (lane & 15);
+      const float swv = swrow[kb];
+      float sc[C::TM];
 #pragma unroll
-      for (int tm = 0; tm < C::TM; ++tm) p[tm] = mfma_fp8_16x16x128(af, bf[tm]);
+      for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sts[tm * 16] * swv;
+
+      const uint8_t* sta = st + C::kWBytes + wm * C::WTM * 128;
+      const uint8_t* stw = st + wn * C::WTN * 128;
+      // first weight fragment, then the activation fragments in the order the
+      // first MFMAs consume them (LDS returns in order, so each MFMA waits only
+      // for its own operands); weight fragments are double-buffered: the next
+      // sub-tile's read is in flight while this one's MFMAs run
+      v8i32 af = lds_frag2(stw, f0, f1);
+      v8i32 bf[C::TM];
 #pragma unroll
-      for (int tm = 0; tm < C::TM; ++tm)
+      for (int tm = 0; tm < C::TM; ++tm) bf[tm] = lds_frag2(sta + tm * 16 * 128, f0, f1);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[tn][tm][r] = __builtin_fmaf(p[tm][r], sc[tm], acc[tn][tm][r]);
-      af = af_next;
+      for (int tn = 0; tn < C::TN; ++tn) {
+#pragma unroll
+        for (int i = 0; i < C::kLoadsPerWave; ++i) {
+          if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill) {
+            const int o = wave + i * C::kWaves;
+            uint32_t off = goff[i];
+            if constexpr (kCross) off = last ? goff_n[i] : goff[i];
+            lds_dma16((o < C::BN / 8 ? dwb : dab) + off, dslot + o * 1024);
+          }
+        }
+        if (tn == 0 && sdma && refill) lds_dma4(dsa, dslot + C::kWBytes + C::kABytes + wave * 256);
+        v8i32 af_next = af;
+        if (tn + 1 < C::TN) af_next = lds_frag2(stw + (tn + 1) * 16 * 128, f0, f1);
+        // all MFMAs of the sub-tile row first (independent results in flight),
+        // then their scale FMAs
+        v4f32 p[C::TM];
+#pragma unroll
+        for (int tm = 0; tm < C::TM; ++tm) p[tm] = mfma_fp8_16x16x128(af, bf[tm]);
+#pragma unroll
+        for (int tm = 0; tm < C::TM; ++tm)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[tn][tm][r] = __builtin_fmaf(p[tm][r], sc[tm], acc[tn][tm][r]);
+        af = af_next;
+      }
+      slot ^= 1;
     }
 
-  }
-  // (the last iteration waited for every DMA: nothing is in flight here)
-
-  if constexpr (kPartial) {
-    // ---- split-K partial: the fp32 sums, four consecutive n per lane (16 bytes)
+    // ---- tile end.  The slot of the last K step (slot ^ 1 now) is free once
+    //      every wave is past the barrier below; with kCross the other holds
+    //      the next tile's first K block (in flight).
+    if constexpr (kPartial) {
+      // split-K partial: the fp32 sums, four consecutive n per lane (16 bytes)
 #pragma unroll
-    for (int tn = 0; tn < C::TN; ++tn) {
-      const int nl = wn * C::WTN + tn * 16 + 4 * fg;
+      for (int tn = 0; tn < C::TN; ++tn) {
+        const int nl = wn * C::WTN + tn * 16 + 4 * fg;
 #pragma unroll
-      for (int tm = 0; tm < C::TM; ++tm) {
-        const int ml = wm * C::WTM + tm * 16 + frow;
-        if (ml < m_valid && nl < n_valid)
-          *reinterpret_cast<v4f32*>(part + (row_lo + ml) * ldp + n0 + nl) = acc[tn][tm];
+        for (int tm = 0; tm < C::TM; ++tm) {
+          const int ml = wm * C::WTM + tm * 16 + frow;
+          if (ml < cur.m_valid && nl < n_valid)
+            *reinterpret_cast<v4f32*>(part + (int64_t)(cur.row_lo + ml) * N + cur.n0 + nl) = acc[tn][tm];
+        }
+      }
+    } else {
+      // fp32 -> bf16 (RNE), staged in LDS, then full 16-byte chunks of whole
+      // output rows with streaming stores.  Direct 8-byte stores from the MFMA
+      // layout wrote partial cache lines (1.6x the output bytes reached HBM)
+      // and let the output displace the operands in the memory-side cache.
+      // Staging layout: rows of BN bf16; 16-byte chunk c of row r (counted
+      // within the row group) sits at c ^ (r & 15), so the 16 rows of one
+      // fragment store, and the rows of one read-back wave instruction, spread
+      // evenly over the 64 banks.  Row groups of kRows rows fit one slot (or,
+      // without kCross, the whole ring).
+      constexpr int kRowBytes = C::BN * 2;
+      constexpr int kChunks = kRowBytes / 16;
+      constexpr int kSpace = kCross ? C::kStageBytes : C::kLdsBytes;
+      constexpr int kRowsFit = kSpace / kRowBytes;
+      constexpr int kRows = kRowsFit >= C::BM ? C::BM : (kRowsFit / C::WTM) * C::WTM;
+      static_assert(kChunks >= 16 && kRows >= C::WTM && C::BM % kRows == 0, "bf16 staging must fit");
+      uint8_t* stage = kCross ? lds + (slot ^ 1) * C::kStageBytes : lds;
+#pragma unroll
+      for (int g0 = 0; g0 < C::BM; g0 += kRows) {
+        lds_barrier();                       // the staging space is free (last K step / previous group)
+        if (wm * C::WTM >= g0 && wm * C::WTM < g0 + kRows) {
+#pragma unroll
+          for (int tn = 0; tn < C::TN; ++tn) {
+            const int nl = wn * C::WTN + tn * 16 + 4 * fg;
+#pragma unroll
+            for (int tm = 0; tm < C::TM; ++tm) {
+              const int ml = wm * C::WTM + tm * 16 + frow - g0;
+              uint2 o;
+              o.x = f32_to_bf16_rne(acc[tn][tm][0]) | (f32_to_bf16_rne(acc[tn][tm][1]) << 16);
+              o.y = f32_to_bf16_rne(acc[tn][tm][2]) | (f32_to_bf16_rne(acc[tn][tm][3]) << 16);
+              *reinterpret_cast<uint2*>(stage + ml * kRowBytes + (((nl >> 3) ^ (ml & 15)) << 4) + ((nl >> 2) & 1) * 8) = o;
+            }
+          }
+        }
+        lds_barrier();
+        const int c = t % kChunks;             // this thread's chunk of every row it writes
+#pragma unroll 4
+        for (int r = t / kChunks; r < kRows; r += C::kThreads / kChunks) {
+          if (g0 + r < cur.m_valid && c * 8 < n_valid) {
+            const uint4 v = *reinterpret_cast<const uint4*>(stage + r * kRowBytes + ((c ^ (r & 15)) << 4));
+            store_stream16(y + (int64_t)(cur.row_lo + g0 + r) * ldy + cur.n0 + c * 8, v);
+          }
+        }
       }
     }
-    return;
-  }
 
-  // ---- epilogue: fp32 -> bf16 (RNE) into a copy of the whole tile in LDS (the
-  //      ring is free once every wave is past its last K step), then each
-  //      workgroup writes full 16-byte chunks of whole output rows with
-  //      streaming stores.  Direct 8-byte stores from the MFMA layout wrote
-  //      partial cache lines (1.6x the output bytes reached HBM) and let the
-  //      output displace the operands in the memory-side cache.
-  //      LDS layout: BM rows of BN bf16; 16-byte chunk c of row r sits at
-  //      c ^ (r & 15), so the 16 rows of one fragment store, and the two rows
-  //      of one read-back wave instruction, spread evenly over the 64 banks.
-  constexpr int kRowBytes = C::BN * 2;
-  constexpr int kChunks = kRowBytes / 16;
-  static_assert(kChunks >= 16 && C::BM * kRowBytes <= C::kLdsBytes, "the bf16 tile must fit in the LDS ring");
-  __syncthreads();
+    if constexpr (!kCross) {
+      break;                                   // one tile per workgroup
+    } else {
+      // (the next step's top barrier orders the staging reads before the slot is refilled)
+      if (!has_nxt) break;
+      cur = nxt;
 #pragma unroll
-  for (int tn = 0; tn < C::TN; ++tn) {
-    const int nl = wn * C::WTN + tn * 16 + 4 * fg;
-#pragma unroll
-    for (int tm = 0; tm < C::TM; ++tm) {
-      const int ml = wm * C::WTM + tm * 16 + frow;
-      uint2 o;
-      o.x = f32_to_bf16_rne(acc[tn][tm][0]) | (f32_to_bf16_rne(acc[tn][tm][1]) << 16);
-      o.y = f32_to_bf16_rne(acc[tn][tm][2]) | (f32_to_bf16_rne(acc[tn][tm][3]) << 16);
-      *reinterpret_cast<uint2*>(lds + ml * kRowBytes + (((nl >> 3) ^ (ml & 15)) << 4) + ((nl >> 2) & 1) * 8) = o;
+      for (int i = 0; i < C::kLoadsPerWave; ++i) goff[i] = goff_n[i];
+      has_nxt = jobs.next(nxt);
+      if (has_nxt) dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid);
     }
   }
-  __syncthreads();
-  const int c = t % kChunks;                    // this thread's chunk of every row it writes
-#pragma unroll 4
-  for (int r = t / kChunks; r < C::BM; r += C::kThreads / kChunks) {
-    if (r < m_valid && c * 8 < n_valid) {
-      const uint4 v = *reinterpret_cast<const uint4*>(lds + r * kRowBytes + ((c ^ (r & 15)) << 4));
-      store_stream16(y + (row_lo + r) * ldy + n0 + c * 8, v);
-    }
-  }
+  // (the last step of the last tile issued no DMA: nothing is in flight here)
 }
 
 }  // namespace fp8rl

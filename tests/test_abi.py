@@ -129,6 +129,7 @@ def test_grouped_gemm_argument_errors(lib):
     assert f(A16, A16, 8, A16, A16, A16, 0, 8, A16, 128, 128, None) == INVALID    # no groups
     assert f(A16, A16, 8, A16, A16, A16, 2, -1, A16, 128, 128, None) == INVALID
     assert f(A16, A16, 8, A16, A16, A16, 2, 8, A16, 192, 128, None) == SHAPE
+    assert f(A16, A16, 8, A16, A16, A16, 1025, 8, A16, 128, 128, None) == SHAPE   # over 1024 experts
     assert f(A16, A16, 7, A16, A16, A16, 2, 8, A16, 128, 128, None) == INVALID    # ld_sa < R
     assert f(A16, A16, 8, A16, A16, None, 2, 8, A16, 128, 128, None) == INVALID
     assert f(A16, A16, 8, A16, A16, A16 + 2, 2, 8, A16, 128, 128, None) == MISALIGNED
