@@ -35,11 +35,11 @@ __device__ __forceinline__ int xcd_contiguous(int id, int total) {
   return x * q + min(x, r) + j;
 }
 
-__device__ __forceinline__ int band_tile(int t, int tiles_m, int tiles_n) {
-  const int band = t / (kGroupM * tiles_n);
-  const int first_m = band * kGroupM;
-  const int gm = min(tiles_m - first_m, kGroupM);
-  const int in_band = t - band * kGroupM * tiles_n;
+__device__ __forceinline__ int band_tile(int t, int tiles_m, int tiles_n, int group_m = kGroupM) {
+  const int band = t / (group_m * tiles_n);
+  const int first_m = band * group_m;
+  const int gm = min(tiles_m - first_m, group_m);
+  const int in_band = t - band * group_m * tiles_n;
   const int tile_m = first_m + in_band % gm;
   const int tile_n = in_band / gm;
   return tile_n * tiles_m + tile_m;
@@ -160,9 +160,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 // first builds, in LDS, the first m tile and the first row of every expert
 // from the device offsets (one prefix scan by wave 0), then runs tiles
 // v = b, b + gridDim.x, ... of the (m tile, n tile) grid, renumbered so that
-// each XCD walks a contiguous range with the m tile fastest: the m tiles of one
-// expert that share a weight slab run on the same XCD and read it from its L2.
+// each XCD walks a contiguous range in bands of kGroupMoe m tiles (m fastest
+// inside a band): an XCD's concurrent tiles share their activation rows across
+// the n tiles and, within an expert, its weight slab, both from its L2.
 constexpr int kMaxExperts = 1024;          // table capacity (LDS: 8 KiB)
+constexpr int kGroupMoe = 2;               // m tiles per band (measured: 2-4 best, 6-10% over m-fastest)
 
 template <class C>
 struct GroupedJobs {
@@ -172,10 +174,10 @@ struct GroupedJobs {
   int64_t N, K;
   __device__ bool next(TileJob& j) {
     if (v >= real_m * tiles_n) return false;
-    const int lin = xcd_contiguous(v, real_m * tiles_n);
+    const int bt = band_tile(xcd_contiguous(v, real_m * tiles_n), real_m, tiles_n, kGroupMoe);
     v += stride;
-    const int target = lin % real_m;
-    const int tile_n = lin / real_m;
+    const int target = bt % real_m;
+    const int tile_n = bt / real_m;
     // e = (number of experts whose first m tile is <= target) - 1: the last
     // such expert owns the tile (empty experts share their start with the next)
     const int lane = threadIdx.x & 63;
@@ -266,7 +268,8 @@ hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, con
   const int64_t max_tiles_m = rows / C::BM + g;        // upper bound on the real m tiles
   const int64_t tiles_n = (n + C::BN - 1) / C::BN;
   const int64_t total = max_tiles_m * tiles_n;
-  const int64_t slots = (int64_t)kCus * per_cu<C, 2 * 4 * (kMaxExperts + 1)>();
+  // persistent grid with the cross-tile pipeline, else one workgroup per tile
+  const int64_t slots = kCrossTiles<C> ? (int64_t)kCus * per_cu<C, 2 * 4 * (kMaxExperts + 1)>() : total;
   hipLaunchKernelGGL(grouped_gemm_w8a8_block_kernel<C>, dim3((unsigned)(total < slots ? total : slots)),
                      dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw, sw, offsets, (int)g, y, n, k,
                      (int)tiles_n);
