@@ -115,6 +115,17 @@ def test_gemm_shapes(fp8rl, m, n, k, pads):
     check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"{m}x{n}x{k}")
 
 
+@pytest.mark.parametrize("m,n,k", [(1000, 16384, 128), (1500, 8192, 384)])
+def test_gemm_many_tiles_per_workgroup(fp8rl, m, n, k):
+    """More 128x128 tiles than the persistent grid has workgroups (512): each workgroup
+    runs several tiles through one pipeline, with ragged last rows; K = 128 makes every
+    K step a tile boundary."""
+    announce(f"gemm persistent m={m} n={n} k={k}")
+    qa, sa, qw, sw = quantised_operands(m, n, k, m + n + k)
+    y = run_dense(fp8rl, qa, sa, qw, sw)
+    check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"{m}x{n}x{k}")
+
+
 def test_gemm_full_range_codes_within_accumulation_bound(fp8rl):
     """Uniformly random codes over the whole E4M3 range (products up to 448^2 with
     heavy cancellation inside a K block).
@@ -321,6 +332,29 @@ def test_grouped_many_experts_matches_dense_per_expert(fp8rl):
     sa, sw = rand_scales((k // 128, r), rng), rand_scales((g, n // 128, k // 128), rng)
     y = run_grouped(fp8rl, qa, sa, qw, sw, offsets)
     check(y, gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, offsets), "grouped 70")
+
+
+@pytest.mark.parametrize("k", [128, 384])
+def test_grouped_many_tiles_per_workgroup(fp8rl, k):
+    """Over 512 expert tiles (several per persistent workgroup), ragged experts, empty
+    experts at both ends, 1 and 3 K blocks per tile."""
+    announce(f"grouped gemm persistent k={k}")
+    rng = np.random.default_rng(k)
+    g, n = 96, 640
+    counts = rng.integers(0, 400, size=g)
+    counts[[0, 17, 95]] = 0
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    r = int(offsets[-1])
+    tiles = int(sum((c + 127) // 128 for c in counts)) * (n // 128)
+    assert tiles > 512, tiles
+    # realistic operands (bf16 N(0,1) activations, N(0,0.02) weights) quantised by the oracle
+    a16 = torch.from_numpy(rng.standard_normal((r, k)).astype(np.float32)).to(torch.bfloat16)
+    w16 = torch.from_numpy((rng.standard_normal((g * n, k)) * 0.02).astype(np.float32)).to(torch.bfloat16)
+    qa, sa = cref.quant_act_token_group128(u16(a16))
+    qw, sw = cref.quant_weight_block128(u16(w16))
+    qw, sw = qw.reshape(g, n, k), sw.reshape(g, n // 128, k // 128)
+    y = run_grouped(fp8rl, qa, sa, qw, sw, offsets)
+    check(y, gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, offsets), f"grouped {g} experts k={k}")
 
 
 @pytest.mark.parametrize("which", ["gate_up", "down"])
