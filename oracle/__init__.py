@@ -13,6 +13,10 @@ This package is a plain, slow, obviously-correct restatement of what the paper
 * ``gemm``  -- the blockwise-scaled FP8 GEMM, dense and grouped by expert
   (section 2.1.4 / section 2.1.1 quantisation scope incl. MoE fc1/fc2),
   evaluated as dequantise-then-matmul in fp64.
+* ``act``   -- the down projection's input: SiLU(gate) * up rounded to bf16,
+  then 1x128 group quantisation (section 2.1.1: down_proj / fc2 are quantised
+  like every linear, activations dynamically), and the row gather of quantised
+  activations that MoE dispatch needs.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import, call or execute anything in this package.  The HIP
@@ -20,4 +24,4 @@ product path never does; it shares no code, table or constant generator with
 this package.  Everything here is numpy on the CPU (plus one small C file,
 ``e4m3_sweep.c``, used only by the exhaustive element-map test).
 """
-from . import e4m3, quant, gemm  # noqa: F401
+from . import e4m3, quant, gemm, act  # noqa: F401
