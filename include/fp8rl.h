@@ -167,6 +167,51 @@ int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld
                                   int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
                                   void* stream);
 
+/*
+ * Down-projection input of the gated MLP, quantised (section 2.1.1: down_proj /
+ * MoE fc2 are quantised like every linear layer, their activations dynamically
+ * with 1x128 groups; section 3.1).  From the fused gate_up output:
+ *
+ *   h[t][c] = bf16_rne( SiLU(gu[t][c]) * gu[t][inter + c] ),  SiLU(g) = g / (1 + e^-g)
+ *
+ * evaluated in fp32 and rounded once, then quantised exactly as
+ * fp8rl_quant_act_token_group128 quantises a bf16 input (the codes and scales
+ * are bit-identical to running that entry point on h).
+ *
+ * gu     [m][ld_gu] bf16: columns 0..inter-1 gate, inter..2*inter-1 up
+ * q      [m][ldq]  E4M3 codes of h out
+ * scale  [inter/128][ld_scale] fp32 out, token index contiguous (as above)
+ * h      [m][ldh]  bf16 h out, or NULL to skip writing it (ldh then ignored)
+ * inter  multiple of 128 (else FP8RL_ERR_UNSUPPORTED_SHAPE); m == 0 is a no-op
+ * Alignment: gu, q, h 16-byte aligned; ld_gu % 8 == 0; ldh % 8 == 0; ldq % 16 == 0;
+ * scale 4-byte aligned.  ld_gu >= 2*inter, ldq >= inter, ldh >= inter, ld_scale >= m.
+ */
+int fp8rl_silu_mul_quant_group128(const uint16_t* gu, int64_t m, int64_t inter, int64_t ld_gu,
+                                  uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
+                                  uint16_t* h, int64_t ldh, void* stream);
+
+/*
+ * Row gather of quantised activations (MoE dispatch: each token's row goes to the
+ * rows of its experts).  Per-token 1x128 quantisation commutes with copying rows
+ * (section 2.1.1, dynamic per-token activation scales), so tokens are quantised
+ * once and gathered:
+ *
+ *   q_dst[r][:] = q_src[index[r]][:],   s_dst[g*ld_s_dst + r] = s_src[g*ld_s_src + index[r]]
+ *
+ * q_src  [src_rows][ldq_src] E4M3; s_src [k/128][ld_s_src] fp32 (token index contiguous)
+ * index  DEVICE int32 [rows], each in [0, src_rows) (precondition, not checked:
+ *        an index outside is clamped into range, so it reads a wrong row but
+ *        never outside the source)
+ * q_dst  [rows][ldq_dst] out; s_dst [k/128][ld_s_dst] out
+ * k multiple of 128; rows == 0 is a no-op; src_rows >= 1 when rows > 0.
+ * Destination and source must not overlap.
+ * Alignment: q_src, q_dst 16-byte aligned; ldq_src % 16 == 0; ldq_dst % 16 == 0;
+ * s_src, s_dst 4-byte aligned.  ldq_* >= k, ld_s_src >= src_rows, ld_s_dst >= rows.
+ */
+int fp8rl_gather_rows_fp8(const uint8_t* q_src, int64_t ldq_src, const float* s_src, int64_t ld_s_src,
+                          int64_t src_rows, const int32_t* index, int64_t rows, int64_t k,
+                          uint8_t* q_dst, int64_t ldq_dst, float* s_dst, int64_t ld_s_dst, void* stream);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* fp8rl_status_string(int status);
 

@@ -24,9 +24,10 @@ __all__ = [
     "fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
     "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
     "fp8rl_gemm_w8a8_block_workspace_size", "fp8rl_gemm_w8a8_block_ws",
+    "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8",
     "fp8rl_status_string", "fp8rl_version",
     "quant_weight_block128", "quant_act_token_group128", "gemm_w8a8_block",
-    "grouped_gemm_w8a8_block", "linear_w8a8",
+    "grouped_gemm_w8a8_block", "silu_mul_quant_group128", "gather_rows_fp8", "linear_w8a8",
 ]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfp8rl.so")
@@ -62,6 +63,8 @@ def _load():
         "fp8rl_gemm_w8a8_block": [P, I, P, I, P, I, P, P, I, I, I, I, P],
         "fp8rl_grouped_gemm_w8a8_block": [P, P, I, P, P, P, I, I, P, I, I, P],
         "fp8rl_gemm_w8a8_block_ws": [P, I, P, I, P, I, P, P, I, I, I, I, P, I, P],
+        "fp8rl_silu_mul_quant_group128": [P, I, I, I, P, I, P, I, P, I, P],
+        "fp8rl_gather_rows_fp8": [P, I, P, I, I, P, I, I, P, I, P, I, P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -276,11 +279,81 @@ def fp8rl_grouped_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.
     return y
 
 
+def fp8rl_silu_mul_quant_group128(gu: torch.Tensor, q: torch.Tensor | None = None,
+                                  scale: torch.Tensor | None = None, ld_scale: int | None = None,
+                                  h: torch.Tensor | None = None, want_h: bool = False, stream=None):
+    """bf16 gate_up [M][2I] ([gate | up]) -> (E4M3 codes of h [M][I], fp32 scales
+    [I/128][ld_scale], h or None) with h = bf16(SiLU(gate) * up).  h is written only
+    when a tensor is passed or want_h is set."""
+    if gu.dtype != torch.bfloat16 or gu.dim() != 2:
+        raise TypeError("gu must be a 2-D bfloat16 tensor")
+    m, two_i = gu.shape
+    if two_i % 2:
+        raise ValueError("gate_up must have an even number of columns")
+    inter = two_i // 2
+    if scale is not None and ld_scale is None:
+        ld_scale = scale.stride(0) if scale.dim() == 2 else m
+    if ld_scale is None:
+        ld_scale = m
+    if q is None:
+        q = torch.empty((m, inter), dtype=torch.uint8, device=gu.device)
+    if scale is None:
+        scale = torch.empty((inter // 128, ld_scale), dtype=torch.float32, device=gu.device)
+    if h is None and want_h:
+        h = torch.empty((m, inter), dtype=torch.bfloat16, device=gu.device)
+    q = _u8(q)
+    _dev(gu, q, scale, *([h] if h is not None else []))
+    if scale.dtype != torch.float32 or scale.numel() < (inter // 128) * ld_scale and m > 0:
+        raise ValueError("scale must be fp32 with at least [I/128][ld_scale] elements")
+    if h is not None and (h.dtype != torch.bfloat16 or h.dim() != 2 or tuple(h.shape) != (m, inter)):
+        raise ValueError("h must be bf16 [M][I]")
+    hp, ldh = (h.data_ptr(), _ld(h) if m else inter) if h is not None else (None, 0)
+    st = load().fp8rl_silu_mul_quant_group128(gu.data_ptr(), m, inter, _ld(gu) if m else two_i, q.data_ptr(),
+                                           _ld(q) if m else inter, scale.data_ptr(), ld_scale, hp, ldh,
+                                           _stream(stream))
+    _check("fp8rl_silu_mul_quant_group128", st)
+    return q, scale, h
+
+
+def fp8rl_gather_rows_fp8(q_src: torch.Tensor, s_src: torch.Tensor, index: torch.Tensor,
+                          q_dst: torch.Tensor | None = None, s_dst: torch.Tensor | None = None,
+                          stream=None):
+    """Rows index[r] of quantised activations: q_src [S][K] codes, s_src [K/128][ld >= S]
+    scales -> (q_dst [R][K], s_dst [K/128][ld >= R]).  index: device int32 [R], each
+    in [0, S)."""
+    q_src = _u8(q_src)
+    src_rows, k = q_src.shape
+    if index.dtype != torch.int32 or index.dim() != 1 or not index.is_contiguous():
+        raise ValueError("index must be a contiguous 1-D int32 tensor")
+    rows = index.numel()
+    if s_src.dtype != torch.float32 or s_src.dim() != 2 or s_src.stride(1) != 1 or s_src.size(0) != k // 128:
+        raise ValueError("s_src must be fp32 [K/128][ld >= S]")
+    if q_dst is None:
+        q_dst = torch.empty((rows, k), dtype=torch.uint8, device=q_src.device)
+    if s_dst is None:
+        s_dst = torch.empty((k // 128, rows), dtype=torch.float32, device=q_src.device)
+    q_dst = _u8(q_dst)
+    if s_dst.dtype != torch.float32 or s_dst.dim() != 2 or s_dst.stride(1) != 1 or s_dst.size(0) != k // 128:
+        raise ValueError("s_dst must be fp32 [K/128][ld >= R]")
+    _dev(q_src, s_src, index, q_dst, s_dst)
+    if rows == 0:
+        return q_dst, s_dst
+    ld_s_src = s_src.stride(0) if s_src.size(0) > 1 else s_src.size(1)
+    ld_s_dst = s_dst.stride(0) if s_dst.size(0) > 1 else s_dst.size(1)
+    st = load().fp8rl_gather_rows_fp8(q_src.data_ptr(), _ld(q_src), s_src.data_ptr(), ld_s_src, src_rows,
+                                   index.data_ptr(), rows, k, q_dst.data_ptr(), _ld(q_dst), s_dst.data_ptr(),
+                                   ld_s_dst, _stream(stream))
+    _check("fp8rl_gather_rows_fp8", st)
+    return q_dst, s_dst
+
+
 # short aliases
 quant_weight_block128 = fp8rl_quant_weight_block128
 quant_act_token_group128 = fp8rl_quant_act_token_group128
 gemm_w8a8_block = fp8rl_gemm_w8a8_block
 grouped_gemm_w8a8_block = fp8rl_grouped_gemm_w8a8_block
+silu_mul_quant_group128 = fp8rl_silu_mul_quant_group128
+gather_rows_fp8 = fp8rl_gather_rows_fp8
 
 
 def linear_w8a8(x: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor, stream=None) -> torch.Tensor:

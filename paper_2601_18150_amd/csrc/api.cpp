@@ -82,6 +82,39 @@ int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int6
       fp8rl::launch_quant_act_token_group128(a, m, k, lda, q, ldq, scale, ld_scale, as_stream(stream)));
 }
 
+int fp8rl_silu_mul_quant_group128(const uint16_t* gu, int64_t m, int64_t inter, int64_t ld_gu, uint8_t* q,
+                                  int64_t ldq, float* scale, int64_t ld_scale, uint16_t* h, int64_t ldh,
+                                  void* stream) {
+  if (m < 0 || inter < 0) return FP8RL_ERR_INVALID_ARG;
+  if (inter % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m >= kMaxDim || 2 * inter >= kMaxDim || m * (inter / 128) >= (int64_t(1) << 28))
+    return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (m == 0 || inter == 0) return FP8RL_OK;
+  if (!gu || !q || !scale) return FP8RL_ERR_INVALID_ARG;
+  if (ld_gu < 2 * inter || ldq < inter || ld_scale < m || (h && ldh < inter)) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(gu, 16) || !aligned(q, 16) || !aligned(scale, 4) || ld_gu % 8 || ldq % 16) return FP8RL_ERR_MISALIGNED;
+  if (h && (!aligned(h, 16) || ldh % 8)) return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_silu_mul_quant_group128(gu, m, inter, ld_gu, q, ldq, scale, ld_scale, h,
+                                                          h ? ldh : 0, as_stream(stream)));
+}
+
+int fp8rl_gather_rows_fp8(const uint8_t* q_src, int64_t ldq_src, const float* s_src, int64_t ld_s_src,
+                          int64_t src_rows, const int32_t* index, int64_t rows, int64_t k, uint8_t* q_dst,
+                          int64_t ldq_dst, float* s_dst, int64_t ld_s_dst, void* stream) {
+  if (rows < 0 || k < 0 || src_rows < 0) return FP8RL_ERR_INVALID_ARG;
+  if (k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (rows >= kMaxDim || src_rows >= kMaxDim || k >= kMaxDim || rows * (k / 16) >= (int64_t(1) << 31))
+    return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (rows == 0 || k == 0) return FP8RL_OK;
+  if (src_rows == 0 || !q_src || !s_src || !index || !q_dst || !s_dst) return FP8RL_ERR_INVALID_ARG;
+  if (ldq_src < k || ldq_dst < k || ld_s_src < src_rows || ld_s_dst < rows) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(q_src, 16) || !aligned(q_dst, 16) || ldq_src % 16 || ldq_dst % 16 || !aligned(s_src, 4) ||
+      !aligned(s_dst, 4) || !aligned(index, 4))
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_gather_rows_fp8(q_src, ldq_src, s_src, ld_s_src, index, src_rows, rows, k, q_dst,
+                                                  ldq_dst, s_dst, ld_s_dst, as_stream(stream)));
+}
+
 int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
                           int64_t ldw, const float* sw, uint16_t* y, int64_t ldy, int64_t m, int64_t n,
                           int64_t k, void* stream) {

@@ -15,6 +15,15 @@ hipError_t launch_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t
                                            uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
                                            hipStream_t stream);
 
+hipError_t launch_silu_mul_quant_group128(const uint16_t* gu, int64_t m, int64_t inter, int64_t ld_gu,
+                                          uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
+                                          uint16_t* h, int64_t ldh, hipStream_t stream);
+
+hipError_t launch_gather_rows_fp8(const uint8_t* q_src, int64_t ldq_src, const float* s_src, int64_t ld_s_src,
+                                  const int32_t* index, int64_t src_rows, int64_t rows, int64_t k,
+                                  uint8_t* q_dst, int64_t ldq_dst, float* s_dst, int64_t ld_s_dst,
+                                  hipStream_t stream);
+
 hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
                                   const uint8_t* qw, int64_t ldw, const float* sw,
                                   uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,

@@ -138,7 +138,146 @@ __global__ __launch_bounds__(256) void quant_act_token_group128_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Down-projection input of the gated MLP: h = bf16(SiLU(gate) * up) from the
+// fused gate_up output [gate | up], then the same 1x128 group quantisation.
+// Layout and lane mapping as the activation kernel: 16 lanes per (token,
+// group), each lane 8 elements of gate and the matching 8 of up.
+//
+// h is the correctly rounded bf16 of the exact SiLU(g) * u.  The fast path
+// evaluates it in fp32: expf (a few ulp), 1 + e, the IEEE quotient and the
+// product leave the fp32 result r within 8 fp32 ulps of the exact value when
+// the quotient is a normal number, so r rounds to the same bf16 as the exact
+// value unless its 16 discarded bits lie within kTieGuard of the half-way
+// point 0x8000.  Those rare elements, and every element whose quotient is
+// tiny, zero, infinite or NaN, take the exact path below.  h is written out
+// only when asked for.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kTieGuard = 64;   // fp32 ulps; the error bound above is 8
+
+// |x| rounded to bf16 from fp64, once: to nearest, an exact tie away from zero
+// (tie > 0), toward zero (tie < 0) or to even (tie == 0); NaN gives 0x7FC0.
+__device__ uint32_t f64_to_bf16_tie(double x, int tie) {
+  if (x != x) return 0x7FC0u;
+  const uint32_t sign = __double_as_longlong(x) < 0 ? 0x8000u : 0u;
+  const double a = fabs(x);
+  if (a == 0.0) return sign;
+  if (a >= 0x1p128) return sign | 0x7F80u;
+  int e;
+  frexp(a, &e);                                        // a in [2^(e-1), 2^e)
+  const int q = max(e - 1, -126) - 7;                  // bf16 spacing near a is 2^q
+  const double t = ldexp(a, -q);                       // exact
+  const double lo = floor(t);
+  const double f = t - lo;
+  double n = f > 0.5 ? lo + 1.0 : lo;
+  if (f == 0.5) n = tie > 0 ? lo + 1.0 : tie < 0 ? lo : (fmod(lo, 2.0) == 0.0 ? lo : lo + 1.0);
+  const double r = ldexp(n, q);
+  if (r >= 0x1p128) return sign | 0x7F80u;
+  return sign | (__float_as_uint((float)r) >> 16);    // exact: at most 8 significant bits
+}
+
+// The exact path.  For g != 0 the exact value is never a bf16 tie, but in two
+// limits it lies closer to an exactly representable product than fp64 can
+// resolve, so the product is rounded with the side of the tie given by the
+// sign of the deviation:
+//   |g| <= 2^-20: SiLU(g) u = (g u / 2)(1 + tanh(g / 2)), within 2^-21 of the
+//                 16-bit product g u / 2: a tie goes away from zero for g > 0,
+//                 toward zero for g < 0;
+//   g >= 16:      SiLU(g) u = g u (1 - 1 / (1 + e^g)), within 2^-23 of g u: a
+//                 tie goes toward zero.
+// Between them the fp64 evaluation is never within 2^-48 of a bf16 rounding
+// boundary (checked over every gate bit pattern and up significand), far
+// beyond its few-ulp error, so its nearest-even rounding is the exact one.
+__device__ __noinline__ uint32_t silu_mul_bf16_exact(float g, float u) {
+  const double gd = g, ud = u;
+  if (fabsf(g) <= 0x1p-20f) return f64_to_bf16_tie(gd * ud * 0.5, g > 0.0f ? 1 : g < 0.0f ? -1 : 0);
+  if (g >= 16.0f) return f64_to_bf16_tie(gd * ud, -1);
+  return f64_to_bf16_tie(gd / (1.0 + exp(-gd)) * ud, 0);
+}
+
+__device__ __forceinline__ uint32_t silu_mul_bf16(uint32_t g16, uint32_t u16) {
+  const float g = __uint_as_float(g16 << 16);
+  const float u = __uint_as_float(u16 << 16);
+  const float q = g / (1.0f + expf(-g));
+  const float r = q * u;
+  const uint32_t low = __float_as_uint(r) & 0xFFFFu;
+  const bool near_tie = low - (0x8000u - kTieGuard) <= 2u * kTieGuard;
+  if (near_tie || !(fabsf(q) >= 0x1p-120f) || !(fabsf(r) <= 0x1.fffffep127f)) return silu_mul_bf16_exact(g, u);
+  return f32_to_bf16_rne(r);
+}
+
+__global__ __launch_bounds__(256) void silu_mul_quant_group128_kernel(
+    const uint16_t* __restrict__ gu, int64_t ld_gu, int64_t inter, uint8_t* __restrict__ q, int64_t ldq,
+    float* __restrict__ scale, int64_t ld_scale, uint16_t* __restrict__ h, int64_t ldh, int64_t units, int ng) {
+  const int t = threadIdx.x;
+  const int64_t unit = (int64_t)blockIdx.x * 16 + (t >> 4);
+  const bool valid = unit < units;
+  const int64_t u = valid ? unit : units - 1;      // keep every lane in bounds
+  const int64_t row = u / ng;
+  const int g = (int)(u - row * ng);
+  const int chunk = t & 15;
+  const uint16_t* src = gu + row * ld_gu + g * 128 + chunk * 8;
+  const uint4 vg = *reinterpret_cast<const uint4*>(src);
+  const uint4 vu = *reinterpret_cast<const uint4*>(src + inter);
+  uint4 v;
+  v.x = silu_mul_bf16(vg.x & 0xFFFFu, vu.x & 0xFFFFu) | (silu_mul_bf16(vg.x >> 16, vu.x >> 16) << 16);
+  v.y = silu_mul_bf16(vg.y & 0xFFFFu, vu.y & 0xFFFFu) | (silu_mul_bf16(vg.y >> 16, vu.y >> 16) << 16);
+  v.z = silu_mul_bf16(vg.z & 0xFFFFu, vu.z & 0xFFFFu) | (silu_mul_bf16(vg.z >> 16, vu.z >> 16) << 16);
+  v.w = silu_mul_bf16(vg.w & 0xFFFFu, vu.w & 0xFFFFu) | (silu_mul_bf16(vg.w >> 16, vu.w >> 16) << 16);
+  const uint32_t m = row16_max(amax16_of(v));
+  const BlockScale bs = qmath::block_scale(m);
+  uint2 c = bs.prescaled ? quant8<true>(v, bs) : quant8<false>(v, bs);
+  if (valid) {
+    *reinterpret_cast<uint2*>(q + row * ldq + g * 128 + chunk * 8) = c;
+    if (chunk == 0) scale[(int64_t)g * ld_scale + row] = bs.scale;
+    if (h) *reinterpret_cast<uint4*>(h + row * ldh + g * 128 + chunk * 8) = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Gather of quantised activation rows: dst row r = src row index[r] (codes and
+// the row's group scales).  One thread per 16-byte chunk of a row; the thread
+// holding the first chunk of a 128-wide group also copies its scale.  Indices
+// outside [0, src_rows) are clamped (a violated precondition, but never an
+// out-of-bounds read).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void gather_rows_fp8_kernel(
+    const uint8_t* __restrict__ q_src, int64_t ldq_src, const float* __restrict__ s_src, int64_t ld_s_src,
+    const int32_t* __restrict__ index, int64_t src_rows, int64_t rows, int64_t chunks,
+    uint8_t* __restrict__ q_dst, int64_t ldq_dst, float* __restrict__ s_dst, int64_t ld_s_dst) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * chunks) return;
+  const int64_t r = i / chunks;
+  const int64_t c = i - r * chunks;
+  const int64_t src = min(max((int64_t)index[r], (int64_t)0), src_rows - 1);
+  *reinterpret_cast<uint4*>(q_dst + r * ldq_dst + c * 16) =
+      *reinterpret_cast<const uint4*>(q_src + src * ldq_src + c * 16);
+  if ((c & 7) == 0) s_dst[(c >> 3) * ld_s_dst + r] = s_src[(c >> 3) * ld_s_src + src];
+}
+
 }  // namespace
+
+hipError_t launch_silu_mul_quant_group128(const uint16_t* gu, int64_t m, int64_t inter, int64_t ld_gu,
+                                          uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
+                                          uint16_t* h, int64_t ldh, hipStream_t stream) {
+  const int ng = (int)(inter / 128);
+  const int64_t units = m * ng;
+  const int64_t blocks = (units + 15) / 16;
+  hipLaunchKernelGGL(silu_mul_quant_group128_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, gu, ld_gu,
+                     inter, q, ldq, scale, ld_scale, h, ldh, units, ng);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows_fp8(const uint8_t* q_src, int64_t ldq_src, const float* s_src, int64_t ld_s_src,
+                                  const int32_t* index, int64_t src_rows, int64_t rows, int64_t k,
+                                  uint8_t* q_dst, int64_t ldq_dst, float* s_dst, int64_t ld_s_dst,
+                                  hipStream_t stream) {
+  const int64_t chunks = k / 16;
+  const int64_t blocks = (rows * chunks + 255) / 256;
+  hipLaunchKernelGGL(gather_rows_fp8_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, q_src, ldq_src, s_src,
+                     ld_s_src, index, src_rows, rows, chunks, q_dst, ldq_dst, s_dst, ld_s_dst);
+  return hipGetLastError();
+}
 
 hipError_t launch_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
                                         uint8_t* q, int64_t ldq, float* scale, hipStream_t stream) {

@@ -214,6 +214,52 @@ def moe_layer(seed: int = 6, device="cpu", tokens: int = 4096, hidden: int = 204
 
 
 # --------------------------------------------------------------------------
+# gated-MLP gate_up outputs (the down projection's input before SiLU * mul)
+# --------------------------------------------------------------------------
+def gate_up_output(seed: int = 7, device="cpu", m: int = 8192, inter: int = 12288, std_gate: float = 2.0,
+                   std_up: float = 1.0, outlier_cols: int = 16, outlier_gain: float = 24.0) -> torch.Tensor:
+    """bf16 [m][2*inter] = [gate | up]: gate ~N(0, std_gate^2), up ~N(0, std_up^2),
+    `outlier_cols` seeded columns of each half scaled by `outlier_gain` (the
+    channel outliers of LLM activations), a few exact zeros per row."""
+    g = _gen(seed, device)
+    x = torch.randn(m, 2 * inter, generator=g, device=device, dtype=torch.float32)
+    x[:, :inter].mul_(std_gate)
+    x[:, inter:].mul_(std_up)
+    if outlier_cols and m:
+        cols = torch.randint(0, inter, (2, outlier_cols), generator=g, device=device)
+        x[:, cols[0]] *= outlier_gain
+        x[:, inter + cols[1]] *= outlier_gain
+    if m:
+        zr = torch.randint(0, m, (max(1, m // 8),), generator=g, device=device)
+        zc = torch.randint(0, 2 * inter, (max(1, m // 8),), generator=g, device=device)
+        x[zr, zc] = 0.0
+    return x.to(torch.bfloat16)
+
+
+def sweep_silu_pairs(device="cpu", exponent: int | None = 127, seed: int = 8, inter: int = 2048) -> torch.Tensor:
+    """bf16 gate_up [R][2*inter] covering every (gate bit pattern, up significand)
+    pair: element i of the gate half holds bit pattern i mod 2^16, the matching up
+    element the sign and 7 mantissa bits i div 2^16 (2^24 pairs in all, R =
+    2^24 / inter).  The up exponent is `exponent` (biased, 127: |up| in [1, 2)) or,
+    when None, a seeded uniform draw from 1..254 per element."""
+    n = 1 << 24
+    if n % inter:
+        raise ValueError("inter must divide 2^24")
+    i = torch.arange(n, dtype=torch.int32, device=device)
+    gate = i & 0xFFFF
+    sig = i >> 16
+    if exponent is None:
+        e = torch.randint(1, 255, (n,), generator=_gen(seed, device), device=device, dtype=torch.int32)
+    else:
+        e = torch.full_like(i, int(exponent))
+    up = ((sig >> 7) << 15) | (e << 7) | (sig & 0x7F)
+    rows = n // inter
+    both = torch.cat([gate.view(rows, inter), up.view(rows, inter)], dim=1)
+    bits = torch.where(both >= 0x8000, both - 0x10000, both).to(torch.int16)
+    return bits.view(torch.bfloat16)
+
+
+# --------------------------------------------------------------------------
 # exhaustive element-map sweep layouts (bit patterns only)
 # --------------------------------------------------------------------------
 def _sweep_rows(per: int, device) -> torch.Tensor:

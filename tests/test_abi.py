@@ -30,10 +30,11 @@ def lib():
     return fp8rl.load()
 
 
-def test_header_declares_the_four_entry_points():
+def test_header_declares_the_entry_points():
     names = declared_functions()
     for f in ("fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
-              "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block"):
+              "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
+              "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8"):
         assert f in names
 
 
@@ -135,6 +136,41 @@ def test_grouped_gemm_argument_errors(lib):
     assert f(A16, A16, 8, A16, A16, A16 + 2, 2, 8, A16, 128, 128, None) == MISALIGNED
     assert f(A16, A16, 8, A4, A16, A16, 2, 8, A16, 128, 128, None) == MISALIGNED
     assert f(None, None, 0, None, None, None, 2, 0, None, 128, 128, None) == OK
+
+
+def test_silu_mul_quant_argument_errors(lib):
+    f = lib.fp8rl_silu_mul_quant_group128
+    #        gu   m  I    ld_gu q   ldq  s   ld_s h  ldh
+    assert f(A16, -1, 128, 256, A16, 128, A16, 1, None, 0, None) == INVALID
+    assert f(A16, 4, 100, 256, A16, 128, A16, 4, None, 0, None) == SHAPE
+    assert f(A16, 4, 128, 255, A16, 128, A16, 4, None, 0, None) == INVALID       # ld_gu < 2I
+    assert f(A16, 4, 128, 256, A16, 120, A16, 4, None, 0, None) == INVALID       # ldq < I
+    assert f(A16, 4, 128, 256, A16, 128, A16, 3, None, 0, None) == INVALID       # ld_scale < m
+    assert f(A16, 4, 128, 256, A16, 128, A16, 4, A16, 64, None) == INVALID       # ldh < I
+    assert f(None, 4, 128, 256, A16, 128, A16, 4, None, 0, None) == INVALID
+    assert f(A16 + 8, 4, 128, 256, A16, 128, A16, 4, None, 0, None) == MISALIGNED
+    assert f(A16, 4, 128, 260, A16, 128, A16, 4, None, 0, None) == MISALIGNED    # ld_gu % 8
+    assert f(A16, 4, 128, 256, A16, 136, A16, 4, None, 0, None) == MISALIGNED    # ldq % 16
+    assert f(A16, 4, 128, 256, A16, 128, A16, 4, A16 + 8, 128, None) == MISALIGNED
+    assert f(A16, 4, 128, 256, A16, 128, A16, 4, A16, 132, None) == MISALIGNED   # ldh % 8
+    assert f(None, 0, 128, 256, None, 128, None, 0, None, 0, None) == OK
+
+
+def test_gather_rows_argument_errors(lib):
+    f = lib.fp8rl_gather_rows_fp8
+    #        qs  ldq  ss  ld_ss S  idx  R  k    qd  ldqd sd  ld_sd
+    assert f(A16, 128, A16, 8, 8, A16, -1, 128, A16, 128, A16, 8, None) == INVALID
+    assert f(A16, 128, A16, 8, 8, A16, 4, 100, A16, 128, A16, 8, None) == SHAPE
+    assert f(A16, 128, A16, 8, 0, A16, 4, 128, A16, 128, A16, 8, None) == INVALID   # rows from nothing
+    assert f(A16, 128, A16, 7, 8, A16, 4, 128, A16, 128, A16, 8, None) == INVALID   # ld_s_src < S
+    assert f(A16, 128, A16, 8, 8, A16, 4, 128, A16, 128, A16, 3, None) == INVALID   # ld_s_dst < R
+    assert f(A16, 120, A16, 8, 8, A16, 4, 128, A16, 128, A16, 8, None) == INVALID   # ldq_src < k
+    assert f(A16, 128, A16, 8, 8, None, 4, 128, A16, 128, A16, 8, None) == INVALID
+    assert f(A16 + 8, 128, A16, 8, 8, A16, 4, 128, A16, 128, A16, 8, None) == MISALIGNED
+    assert f(A16, 136, A16, 8, 8, A16, 4, 128, A16, 128, A16, 8, None) == MISALIGNED
+    assert f(A16, 128, A16, 8, 8, A16 + 2, 4, 128, A16, 128, A16, 8, None) == MISALIGNED
+    assert f(A16, 128, A16 + 2, 8, 8, A16, 4, 128, A16, 128, A16, 8, None) == MISALIGNED
+    assert f(None, 128, None, 0, 0, None, 0, 128, None, 128, None, 0, None) == OK
 
 
 def test_binding_rejects_cpu_tensors():

@@ -1,0 +1,184 @@
+"""GPU parity of the down-projection input step (h = bf16(SiLU(gate) * up), then
+1x128 group quantisation) and of the quantised-row gather, against the CPU
+oracle (section 2.1.1: down_proj / MoE fc2 quantised like every linear, their
+activations dynamically per token and 128-wide group).
+
+h is the correctly rounded bf16 of the exact value on both sides, so h, codes
+and scales are all compared bit for bit; codes and scales only where h is
+finite (NaN / inf activations are outside the quantiser's domain)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import act, cref, quant
+from tests.gpu_util import announce, assert_codes_equal, assert_scales_equal, need_gpu, u8, u16, f32
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def fp8rl():
+    need_gpu()
+    import paper_2601_18150_amd as m
+    m.load()
+    return m
+
+
+def assert_bits_equal(got: np.ndarray, want: np.ndarray, what: str):
+    if not np.array_equal(got, want):
+        bad = np.argwhere(got != want)
+        i = tuple(bad[0])
+        raise AssertionError(f"{what}: {len(bad)} of {want.size} differ; first at {i}: "
+                             f"got {hex(int(got[i]))}, want {hex(int(want[i]))}")
+
+
+def finite_groups(h: np.ndarray) -> np.ndarray:
+    """[M][I/128] mask of groups whose bf16 values are all finite."""
+    m, i = h.shape
+    return ((h & 0x7F80) != 0x7F80).reshape(m, i // 128, 128).all(axis=2)
+
+
+def check_fused(gu_t, inter, q, s, h, ld_scale=None, rows=None, big=False):
+    """Compare GPU (q, s, h) with the oracle on the given rows (all when None)."""
+    gu = u16(gu_t)
+    gq, gs, gh = u8(q), f32(s), u16(h)
+    if rows is not None:
+        gu, gq, gh = gu[rows], gq[rows], gh[rows]
+        gs = gs[:, rows]
+    wh = act.silu_mul_bf16(gu, inter)
+    assert_bits_equal(gh, wh, "h")
+    ok = finite_groups(wh)
+    m = wh.shape[0]
+    if ok.all():
+        wq, ws = (cref if big else quant).quant_act_token_group128(wh)
+        assert_codes_equal(gq, wq, "codes")
+        assert_scales_equal(gs[:, :m], ws[:, :m], "scales")
+        return
+    wq, ws = cref.quant_act_token_group128(np.where(np.repeat(ok, 128, axis=1), wh, 0).astype(np.uint16))
+    mask = np.repeat(ok, 128, axis=1)
+    assert_codes_equal(np.where(mask, gq, 0), np.where(mask, wq, 0), "codes (finite groups)")
+    okt = ok.T
+    assert_scales_equal(np.where(okt, gs[:, :m], 0), np.where(okt, ws[:, :m], 0), "scales (finite groups)")
+
+
+def test_silu_mul_quant_tiny(fp8rl):
+    announce("silu_mul_quant tiny 64x(2x512)")
+    gu = synth.gate_up_output(seed=21, device="cuda", m=64, inter=512)
+    q, s, h = fp8rl.fp8rl_silu_mul_quant_group128(gu, want_h=True)
+    torch.cuda.synchronize()
+    check_fused(gu, 512, q, s, h)
+
+
+@pytest.mark.parametrize("m,inter", [(1, 128), (3, 384), (37, 640), (129, 256), (300, 1536)])
+def test_silu_mul_quant_ragged_and_ld(fp8rl, m, inter):
+    announce(f"silu_mul_quant ragged m={m} inter={inter}, ld_gu > 2I, ldh/ldq > I, ld_scale > m")
+    full = synth.gate_up_output(seed=30 + m, device="cuda", m=m, inter=inter + 64, outlier_cols=4)
+    gu = torch.cat([full[:, :inter], full[:, inter + 64:2 * inter + 64]], dim=1)
+    gpad = torch.zeros((m, 2 * inter + 40), dtype=torch.bfloat16, device="cuda")
+    gpad[:, :2 * inter] = gu
+    ld = m + 3
+    sbuf = torch.full((inter // 128, ld), -7.0, dtype=torch.float32, device="cuda")
+    qbuf = torch.full((m, inter + 32), 0xAB, dtype=torch.uint8, device="cuda")
+    hbuf = torch.full((m, inter + 16), -5.0, dtype=torch.bfloat16, device="cuda")
+    q, s, h = fp8rl.fp8rl_silu_mul_quant_group128(gpad[:, :2 * inter], q=qbuf[:, :inter], scale=sbuf,
+                                                  ld_scale=ld, h=hbuf[:, :inter])
+    torch.cuda.synchronize()
+    check_fused(gu, inter, q, s, h)
+    assert np.all(f32(sbuf)[:, m:] == -7.0), "scale padding columns were written"
+    assert np.all(u8(qbuf[:, inter:]) == 0xAB), "wrote codes past I"
+    assert np.all(f32(hbuf.float()[:, inter:]) == -5.0), "wrote h past I"
+
+
+def test_silu_mul_quant_without_h_matches(fp8rl):
+    announce("silu_mul_quant h=NULL gives the same codes")
+    gu = synth.gate_up_output(seed=22, device="cuda", m=200, inter=768)
+    q1, s1, h = fp8rl.fp8rl_silu_mul_quant_group128(gu, want_h=True)
+    q2, s2, none = fp8rl.fp8rl_silu_mul_quant_group128(gu)
+    torch.cuda.synchronize()
+    assert none is None
+    assert torch.equal(q1, q2) and torch.equal(s1, s2)
+
+
+@pytest.mark.parametrize("exponent", [127, None], ids=["up_in_1_2", "up_random_exponent"])
+def test_silu_mul_exhaustive_pairs(fp8rl, exponent):
+    """Every gate bit pattern against every up significand (2^24 pairs): h bit-exact
+    with the correctly rounded value, including NaN / inf / subnormal gates, exp
+    overflow and bf16 overflow and underflow of the product."""
+    announce(f"silu_mul_quant exhaustive pairs, up exponent {exponent}")
+    gu = synth.sweep_silu_pairs("cuda", exponent=exponent)
+    q, s, h = fp8rl.fp8rl_silu_mul_quant_group128(gu, want_h=True)
+    torch.cuda.synchronize()
+    check_fused(gu, gu.shape[1] // 2, q, s, h, big=True)
+
+
+def test_silu_mul_quant_dense_mlp_full_sampled(fp8rl):
+    """Full Qwen3-8B MLP shape (8192 tokens, intermediate 12288): the whole step runs
+    on the GPU, the oracle checks 256 seeded rows (the step is row-independent)."""
+    announce("silu_mul_quant dense MLP 8192 x (2 x 12288), sampled rows")
+    gu = synth.gate_up_output(seed=23, device="cuda", m=8192, inter=12288)
+    q, s, h = fp8rl.fp8rl_silu_mul_quant_group128(gu, want_h=True)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(23).choice(8192, 256, replace=False))
+    rows[-1] = 8191
+    check_fused(gu, 12288, q, s, h, rows=rows)
+
+
+def test_silu_mul_quant_zero_rows_is_noop(fp8rl):
+    announce("silu_mul_quant m=0")
+    gu = torch.empty((0, 512), dtype=torch.bfloat16, device="cuda")
+    q, s, h = fp8rl.fp8rl_silu_mul_quant_group128(gu, want_h=True)
+    torch.cuda.synchronize()
+    assert q.shape == (0, 256) and h.shape == (0, 256)
+
+
+def test_gather_moe_dispatch_bit_exact(fp8rl):
+    """Qwen3-30B-A3B dispatch: 4096 tokens x 2048 quantised once, gathered to the
+    32768 expert-grouped rows of a Zipf(1.1) top-8 routing."""
+    announce("gather_rows_fp8 MoE dispatch 4096 -> 32768 rows, k=2048")
+    routing = synth.moe_routing(seed=6, tokens=4096, experts=128, topk=8)
+    x_tok = synth.normal_bf16((4096, 2048), 1.0, 6 + 11, "cpu")
+    qo, so = cref.quant_act_token_group128(u16(x_tok))
+    index = routing.token_of_row
+    gq_want, gs_want = act.gather_rows_fp8(qo, so, index.numpy())
+    q = torch.from_numpy(qo).cuda()
+    s = torch.from_numpy(so).cuda()
+    idx = index.to(torch.int32).cuda()
+    gq, gs = fp8rl.fp8rl_gather_rows_fp8(q, s, idx)
+    torch.cuda.synchronize()
+    assert_codes_equal(u8(gq), gq_want, "gathered codes")
+    assert_scales_equal(f32(gs), gs_want, "gathered scales")
+
+
+@pytest.mark.parametrize("src_rows,rows,k", [(1, 5, 128), (7, 3, 384), (300, 1000, 640), (50, 0, 256)])
+def test_gather_ragged_and_ld(fp8rl, src_rows, rows, k):
+    announce(f"gather_rows_fp8 src={src_rows} rows={rows} k={k}, padded lds")
+    rng = np.random.default_rng(src_rows * 1000 + rows)
+    codes = rng.integers(0, 256, (src_rows, k + 48), dtype=np.uint8)
+    scales = rng.standard_normal((k // 128, src_rows + 5)).astype(np.float32)
+    index = rng.integers(0, src_rows, rows).astype(np.int64)
+    qd = torch.full((rows, k + 16), 0xCD, dtype=torch.uint8, device="cuda")
+    sd = torch.full((k // 128, rows + 2), -9.0, dtype=torch.float32, device="cuda")
+    q_src = torch.from_numpy(codes).cuda()[:, :k]
+    s_src = torch.from_numpy(scales).cuda()
+    fp8rl.fp8rl_gather_rows_fp8(q_src, s_src, torch.from_numpy(index.astype(np.int32)).cuda(),
+                                q_dst=qd[:, :k], s_dst=sd)
+    torch.cuda.synchronize()
+    wq, ws = act.gather_rows_fp8(codes[:, :k], scales[:, :src_rows], index)
+    assert_codes_equal(u8(qd)[:, :k], wq, "codes")
+    assert_scales_equal(f32(sd)[:, :rows], ws, "scales")
+    assert np.all(u8(qd)[:, k:] == 0xCD), "wrote past k"
+    assert np.all(f32(sd)[:, rows:] == -9.0), "wrote scale padding"
+
+
+def test_gather_then_gemm_equals_gemm_of_gathered_rows(fp8rl):
+    """Gathering quantised rows and quantising gathered bf16 rows give the same GEMM
+    input, so the grouped GEMM sees identical operands either way."""
+    announce("gather vs quantise-after-gather, 512 tokens -> 1024 rows")
+    x = synth.normal_bf16((512, 1024), 1.0, 40, "cuda")
+    idx = torch.from_numpy(np.random.default_rng(40).integers(0, 512, 1024).astype(np.int32)).cuda()
+    q, s = fp8rl.fp8rl_quant_act_token_group128(x)
+    gq, gs = fp8rl.fp8rl_gather_rows_fp8(q, s, idx)
+    q2, s2 = fp8rl.fp8rl_quant_act_token_group128(x[idx.long()].contiguous())
+    torch.cuda.synchronize()
+    assert torch.equal(gq, q2) and torch.equal(gs, s2)

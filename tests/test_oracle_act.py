@@ -125,3 +125,129 @@ def test_gather_commutes_with_row_quantisation():
     gq, gs = act.gather_rows_fp8(q, s, index)
     wq, ws = quant.quant_act_token_group128(bits[index])
     assert np.array_equal(gq, wq) and np.array_equal(gs.view(np.uint32), ws.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# correct rounding of SiLU(g) * u, checked against 150-digit decimal arithmetic
+# (the decimal module's exp is correctly rounded) and by brute-force nearest
+# ---------------------------------------------------------------------------
+def _exact_silu_mul(g: float, u: float):
+    import decimal
+    ctx = decimal.Context(prec=150)
+    gd, ud = decimal.Decimal(g), decimal.Decimal(u)
+    return ctx.multiply(ctx.divide(gd, ctx.add(1, ctx.exp(-gd))), ud)
+
+
+def _assert_nearest(bits: int, exact) -> None:
+    """bits is the bf16 nearest to `exact` (strictly: the exact value is never a tie)."""
+    import decimal
+    mag = bits & 0x7FFF
+    neg = bool(bits & 0x8000)
+    val = lambda b: decimal.Decimal(float(bf16_value(np.array([b], dtype=np.uint16))[0]))
+    with decimal.localcontext(decimal.Context(prec=200)):    # differences of dyadic values: exact
+        x = -exact if neg else exact
+        if exact == 0:
+            assert mag == 0
+            return
+        assert x > 0, "sign"
+        d = abs(x - val(mag))
+        assert d < abs(x - val(mag + 1)), f"bits {hex(bits)}: the next magnitude is nearer to {exact}"
+        if mag > 0:
+            assert d < abs(x - val(mag - 1)), f"bits {hex(bits)}: the previous magnitude is nearer to {exact}"
+
+
+def _pairs_from_bits(gb, ub):
+    gb = np.asarray(gb, dtype=np.uint16)[None, :]
+    ub = np.asarray(ub, dtype=np.uint16)[None, :]
+    return np.concatenate([gb, ub], axis=1), gb.shape[1]
+
+
+def test_silu_mul_correctly_rounded_random_pairs():
+    """Random finite gate values over the whole useful range (both limits and the
+    fp64-evaluated middle) and random up values: brute-force nearest bf16 of the
+    150-digit value."""
+    rng = np.random.default_rng(11)
+    g = np.concatenate([
+        rng.integers(0x0001, 0x4380, 600),              # positive, up to 256
+        rng.integers(0x8001, 0xC300, 600),              # negative, down to -128
+        rng.integers(0x3400, 0x4200, 300),              # 2^-23 .. 32 (both limits' edges)
+    ]).astype(np.uint16)
+    u = rng.integers(0x0001, 0x7F00, g.size).astype(np.uint16) | (rng.integers(0, 2, g.size) << 15).astype(np.uint16)
+    bits, n = _pairs_from_bits(g, u)
+    h = act.silu_mul_bf16(bits, n)[0]
+    gv, uv = bf16_value(g), bf16_value(u)
+    for i in range(n):
+        _assert_nearest(int(h[i]), _exact_silu_mul(float(gv[i]), float(uv[i])))
+
+
+def _tie_pairs(g_bits):
+    """Pairs (g, u) whose product g u (or g u / 2) is exactly a bf16 rounding tie:
+    u runs over all 128 significands in [1, 2); keep the products with 9 significant
+    bits ending in 1."""
+    gs, us = [], []
+    ub = np.arange(0x3F80, 0x4000, dtype=np.uint16)
+    for gb in g_bits:
+        gv = float(bf16_value(np.array([gb], dtype=np.uint16))[0])
+        for u16 in ub:
+            uv = float(bf16_value(np.array([u16], dtype=np.uint16))[0])
+            m, _ = np.frexp(abs(gv * uv))
+            sig = int(round(m * 2 ** 16))                   # 16 significant bits, exact
+            if sig % (1 << 8) == (1 << 7):                  # 8 kept bits, then exactly one half: a tie
+                gs.append(gb)
+                us.append(u16)
+    return np.array(gs, dtype=np.uint16), np.array(us, dtype=np.uint16)
+
+
+def test_silu_mul_ties_in_the_small_gate_limit():
+    """|g| <= 2^-20: g u / 2 exactly on a bf16 tie; the exact value is off it by the
+    relative amount tanh(g / 2), so it rounds away from zero for g > 0 and toward
+    zero for g < 0 -- checked against the 150-digit value, for both signs of u."""
+    gb = np.array([0x3580, 0x35C0, 0x2E40, 0x1FA0, 0x0C60, 0xB580, 0xB5C0, 0xAE40, 0x8C60, 0x3480], dtype=np.uint16)
+    g, u = _tie_pairs(gb)
+    assert g.size > 20
+    u = np.concatenate([u, u | 0x8000])
+    g = np.concatenate([g, g])
+    bits, n = _pairs_from_bits(g, u)
+    h = act.silu_mul_bf16(bits, n)[0]
+    gv, uv = bf16_value(g), bf16_value(u)
+    for i in range(n):
+        _assert_nearest(int(h[i]), _exact_silu_mul(float(gv[i]), float(uv[i])))
+
+
+def test_silu_mul_ties_in_the_large_gate_limit():
+    """g >= 16: g u exactly on a bf16 tie; SiLU(g) < g, so the exact value rounds
+    toward zero.  Gates from 16 to 200 (e^-200 is still resolved at 150 digits)."""
+    gb = np.array([0x4180, 0x4190, 0x41A0, 0x4240, 0x4280, 0x42C8, 0x4348], dtype=np.uint16)  # 16 .. 200
+    g, u = _tie_pairs(gb)
+    assert g.size > 20
+    bits, n = _pairs_from_bits(g, u)
+    h = act.silu_mul_bf16(bits, n)[0]
+    gv, uv = bf16_value(g), bf16_value(u)
+    for i in range(n):
+        _assert_nearest(int(h[i]), _exact_silu_mul(float(gv[i]), float(uv[i])))
+
+
+def test_silu_mul_fp64_middle_never_near_a_tie():
+    """Between the two limits the oracle trusts fp64 (error a few 2^-53).  Over every
+    finite gate bit pattern there (g > -700: below that the product is far below
+    the smallest bf16 at any up) and every up significand, SiLU(g) u_sig stays more
+    than 2^-47 (in significand units) away from every bf16 rounding boundary, at
+    every number of kept bits from 0 (the smallest subnormal) to 8 (normal
+    numbers); scaling u by a power of two only moves that picture."""
+    gbits = np.arange(0x10000, dtype=np.uint32).astype(np.uint16)
+    with np.errstate(invalid="ignore"):
+        g = bf16_value(gbits)
+    keep = np.isfinite(g) & (np.abs(g) > act.SMALL_G) & (g < act.LARGE_G) & (g > -700.0)
+    g = g[keep]
+    u = 1.0 + np.arange(128, dtype=np.float64) / 128.0
+    with np.errstate(over="ignore"):
+        silu = g / (1.0 + np.exp(-g))
+    worst = np.inf
+    for s in range(9):
+        for j in range(0, 128, 32):
+            x = np.abs(silu[:, None] * u[None, j:j + 32])
+            m, _ = np.frexp(x)
+            y = np.ldexp(m * 2.0, s)                     # significand in [1, 2), times 2^s (exact)
+            dist = np.abs(y - np.floor(y) - 0.5) / 2.0 ** s
+            worst = min(worst, float(dist.min()))
+    assert worst > 2.0 ** -47, worst
