@@ -12,12 +12,14 @@ The JSON line's `value` is the step's effective GEMM throughput (2MNK per step
 is the GEMM kernel alone, timed with HIP events on the stream it runs on.
 `extra` carries the same run's weight-resync figure (36 Qwen3-8B layers, 144
 matrices, GB/s vs HBM), the MoE grouped GEMM (Qwen3-30B-A3B experts), the
-decode linears of 36 distinct Qwen3-8B layers (M=256, weights from HBM), a plain
-device copy, and the rate of a register-fed FP8 MFMA loop with its clock.
+decode linears of 36 distinct Qwen3-8B layers (M=256, weights from HBM), the
+whole FP8 Qwen3-8B MLP (with the same MLP in bf16 through torch beside it) and
+Qwen3-30B-A3B expert block, a plain device copy, and the rate of a register-fed
+FP8 MFMA loop with its clock.
 `cpu_baseline` times the CPU oracle on a bounded row sample of the same step.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload prefill|requant|moe|decode|copy]
+                       [--workload prefill|requant|moe|decode|mlp|moe_block|copy]
                        [--no-cpu-baseline] [--no-extra]
 """
 import argparse
@@ -43,7 +45,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe", "copy"])
+    ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe", "copy", "mlp",
+                                                              "moe_block"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -263,6 +266,126 @@ def moe(args, fp8rl, steps=10, warmup=3):
 
 
 # ---------------------------------------------------------------------------
+# whole FP8 MLP blocks: dense Qwen3-8B MLP and one Qwen3-30B-A3B MoE expert block
+# ---------------------------------------------------------------------------
+def _silu_quant_bytes(m, inter):
+    """Algorithmic HBM bytes of the fused SiLU*mul + quantisation (h not written):
+    read gate and up (bf16), write codes and one fp32 scale per 128 elements."""
+    return m * inter * 4 + m * inter + m * (inter // 128) * 4
+
+
+def mlp(args, fp8rl, steps=10, warmup=3):
+    """Qwen3-8B MLP forward at prefill (8192 tokens): quantise x, gate_up GEMM
+    (N=24576), fused SiLU*mul + 1x128 quantisation, down GEMM (K=12288), all in
+    FP8 with the weights pre-quantised; next to it the same MLP in bf16 through
+    torch (hipBLASLt GEMMs, SiLU and product as separate elementwise kernels)."""
+    m, h, inter = 8192, 4096, 12288
+    x = synth.normal_bf16((m, h), 1.0, 50, "cuda")
+    w_gu = synth.normal_bf16((2 * inter, h), 0.02, 51, "cuda")
+    w_dn = synth.normal_bf16((h, inter), 0.02, 52, "cuda")
+    qgu, sgu = fp8rl.fp8rl_quant_weight_block128(w_gu)
+    qdn, sdn = fp8rl.fp8rl_quant_weight_block128(w_dn)
+    qx = torch.empty((m, h), dtype=torch.uint8, device="cuda")
+    sx = torch.empty((h // 128, m), dtype=torch.float32, device="cuda")
+    gu = torch.empty((m, 2 * inter), dtype=torch.bfloat16, device="cuda")
+    qh = torch.empty((m, inter), dtype=torch.uint8, device="cuda")
+    sh = torch.empty((inter // 128, m), dtype=torch.float32, device="cuda")
+    y = torch.empty((m, h), dtype=torch.bfloat16, device="cuda")
+    timer = KernelTimer()
+
+    def step():
+        with timer.span("quant_act"):
+            fp8rl.fp8rl_quant_act_token_group128(x, q=qx, scale=sx)
+        with timer.span("gemm_gate_up"):
+            fp8rl.fp8rl_gemm_w8a8_block(qx, sx, qgu, sgu, y=gu)
+        with timer.span("silu_mul_quant"):
+            fp8rl.fp8rl_silu_mul_quant_group128(gu, q=qh, scale=sh)
+        with timer.span("gemm_down"):
+            fp8rl.fp8rl_gemm_w8a8_block(qh, sh, qdn, sdn, y=y)
+
+    ms, _ = timed_loop(step, steps, warmup, timer)
+    kern = timer.averages_ms()
+    wt_gu, wt_dn = w_gu.t().contiguous(), w_dn.t().contiguous()
+
+    def step_bf16():
+        g = torch.matmul(x, wt_gu)
+        hh = torch.nn.functional.silu(g[:, :inter]) * g[:, inter:]
+        torch.matmul(hh, wt_dn)
+
+    ms_bf16, _ = timed_loop(step_bf16, steps, warmup, KernelTimer())
+    flops = 2.0 * m * h * 2 * inter + 2.0 * m * inter * h
+    sq = _silu_quant_bytes(m, inter)
+    res = {"workload": f"Qwen3-8B MLP forward, {m} tokens: quant x, gate_up GEMM, fused SiLU*mul+quant, "
+                       f"down GEMM (weights pre-quantised)",
+           "ms_per_step": round(ms, 4), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
+           "bf16_torch_ms_per_step": round(ms_bf16, 4), "speedup_vs_bf16_torch": round(ms_bf16 / ms, 3),
+           "kernels_ms": {k: round(v, 5) for k, v in kern.items()},
+           "silu_mul_quant": {"bytes": sq, "GB/s": round(sq / (kern["silu_mul_quant"] * 1e-3) / 1e9, 1),
+                              "frac_hbm": round(sq / (kern["silu_mul_quant"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}}
+    del x, w_gu, w_dn, qgu, qdn, gu, qh, y, wt_gu, wt_dn
+    torch.cuda.empty_cache()
+    return res
+
+
+def moe_block(args, fp8rl, steps=10, warmup=3):
+    """One Qwen3-30B-A3B expert block (4096 tokens, top-8 of 128 experts, hidden
+    2048, expert intermediate 768) end to end in FP8: quantise the tokens once,
+    gather the quantised rows into expert order, grouped gate_up GEMM, fused
+    SiLU*mul + quantisation, grouped down GEMM."""
+    lay = synth.moe_layer(device="cuda")
+    routing = lay["routing"]
+    off = routing.offsets.to("cuda")
+    idx = routing.token_of_row.to(torch.int32).to("cuda")
+    tokens, hidden = 4096, lay["w_gate_up"].shape[2]
+    x_tok = synth.normal_bf16((tokens, hidden), 1.0, 6 + 11, "cuda")
+    qw = {}
+    for which in ("w_gate_up", "w_down"):
+        g, n, k = lay[which].shape
+        q, s = fp8rl.fp8rl_quant_weight_block128(lay[which].reshape(g * n, k))
+        qw[which] = (q.reshape(g, n, k), s.reshape(g, n // 128, k // 128))
+    inter = lay["w_down"].shape[2]
+    rows = idx.numel()
+    del lay
+    torch.cuda.empty_cache()
+    qx = torch.empty((tokens, hidden), dtype=torch.uint8, device="cuda")
+    sx = torch.empty((hidden // 128, tokens), dtype=torch.float32, device="cuda")
+    qr = torch.empty((rows, hidden), dtype=torch.uint8, device="cuda")
+    sr = torch.empty((hidden // 128, rows), dtype=torch.float32, device="cuda")
+    gu = torch.empty((rows, 2 * inter), dtype=torch.bfloat16, device="cuda")
+    qh = torch.empty((rows, inter), dtype=torch.uint8, device="cuda")
+    sh = torch.empty((inter // 128, rows), dtype=torch.float32, device="cuda")
+    y = torch.empty((rows, hidden), dtype=torch.bfloat16, device="cuda")
+    timer = KernelTimer()
+
+    def step():
+        with timer.span("quant_act"):
+            fp8rl.fp8rl_quant_act_token_group128(x_tok, q=qx, scale=sx)
+        with timer.span("gather_rows"):
+            fp8rl.fp8rl_gather_rows_fp8(qx, sx, idx, q_dst=qr, s_dst=sr)
+        with timer.span("grouped_gate_up"):
+            fp8rl.fp8rl_grouped_gemm_w8a8_block(qr, sr, *qw["w_gate_up"], off, y=gu)
+        with timer.span("silu_mul_quant"):
+            fp8rl.fp8rl_silu_mul_quant_group128(gu, q=qh, scale=sh)
+        with timer.span("grouped_down"):
+            fp8rl.fp8rl_grouped_gemm_w8a8_block(qh, sh, *qw["w_down"], off, y=y)
+
+    ms, _ = timed_loop(step, steps, warmup, timer)
+    kern = timer.averages_ms()
+    flops = 2.0 * rows * hidden * 2 * inter + 2.0 * rows * inter * hidden
+    sq = _silu_quant_bytes(rows, inter)
+    gb = 2 * rows * hidden + 2 * rows * (hidden // 128) * 4
+    res = {"workload": f"Qwen3-30B-A3B expert block, {tokens} tokens x top-8 -> {rows} rows: quant, gather, "
+                       f"grouped gate_up, fused SiLU*mul+quant, grouped down",
+           "ms_per_step": round(ms, 4), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
+           "kernels_ms": {k: round(v, 5) for k, v in kern.items()},
+           "silu_mul_quant": {"bytes": sq, "GB/s": round(sq / (kern["silu_mul_quant"] * 1e-3) / 1e9, 1)},
+           "gather_rows": {"bytes": gb, "GB/s": round(gb / (kern["gather_rows"] * 1e-3) / 1e9, 1)}}
+    del qw, x_tok, qx, qr, gu, qh, y
+    torch.cuda.empty_cache()
+    return res
+
+
+# ---------------------------------------------------------------------------
 # decode linears of one Qwen3-8B layer (M=256): GEMM timing per linear
 # ---------------------------------------------------------------------------
 def decode(args, fp8rl, sweeps=3, warmup=1, layers=synth.QWEN3_8B_LAYERS):
@@ -445,7 +568,7 @@ def main():
             print(json.dumps({"workload": "device-to-device copy of 4 GiB (torch copy_)",
                               "GB/s": hbm_copy_reference()}), flush=True)
             return
-        fn = {"requant": requant, "moe": moe, "decode": decode}[args.workload]
+        fn = {"requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
     out, (a, w) = prefill(args, fp8rl)
@@ -453,7 +576,8 @@ def main():
                 "scaling": "weak", "vs_baseline": None, "data": "synthetic"})
     if not args.no_extra:
         extra = {"weight_resync": requant(args, fp8rl), "moe_grouped": moe(args, fp8rl),
-                 "decode_36_layers": decode(args, fp8rl), "hbm_copy_GB/s": hbm_copy_reference(),
+                 "decode_36_layers": decode(args, fp8rl), "dense_mlp": mlp(args, fp8rl),
+                 "moe_block": moe_block(args, fp8rl), "hbm_copy_GB/s": hbm_copy_reference(),
                  "mfma_probe": mfma_probe()}
         out["extra"] = extra
         out["roofline"]["frac_of_measured_mfma_loop"] = round(

@@ -1,10 +1,16 @@
-// Measurement probe, not part of the FP8 linear-layer path: a loop of
-// independent v_mfma_f32_16x16x128_f8f6f4 instructions fed from registers,
-// which gives the FP8 MFMA rate this GPU sustains (at the clock its power limit
-// allows for pure MFMA work) as a measured reference next to the spec peak.
-// Built into its own library (libfp8rl_probe.so) for bench.py.
+// Measurement probes, not part of the FP8 linear-layer path, built into their
+// own library (libfp8rl_probe.so):
+//  * a loop of independent v_mfma_f32_16x16x128_f8f6f4 instructions fed from
+//    registers, which gives the FP8 MFMA rate this GPU sustains (at the clock
+//    its power limit allows for pure MFMA work) as a measured reference next to
+//    the spec peak;
+//  * the fp32 fast path of the SiLU * up evaluation (silu_math.hpp, the same
+//    code the fused down-projection kernel runs) element by element, so that
+//    its error can be measured against the exact value for every input.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "silu_math.hpp"
 
 namespace {
 
@@ -41,6 +47,16 @@ __global__ __launch_bounds__(256) void mfma_rate_kernel(float* __restrict__ out,
   }
 }
 
+// One thread per element: r = the fast path's fp32 result, q its quotient.
+__global__ __launch_bounds__(256) void silu_fast_kernel(const uint16_t* __restrict__ g, const uint16_t* __restrict__ u,
+                                                        float* __restrict__ r, float* __restrict__ q, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float qi;
+  r[i] = fp8rl::silu::fast(__uint_as_float((uint32_t)g[i] << 16), __uint_as_float((uint32_t)u[i] << 16), qi);
+  q[i] = qi;
+}
+
 }  // namespace
 
 // Enqueue the probe: `blocks` workgroups of 256 threads; out holds blocks*256
@@ -49,4 +65,14 @@ extern "C" int fp8rl_probe_mfma_rate(float* out, unsigned long long* clk, int bl
   if (!out || !clk || blocks <= 0 || iters <= 0) return (int)hipErrorInvalidValue;
   hipLaunchKernelGGL(mfma_rate_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, out, iters, clk);
   return (int)hipGetLastError();
+}
+
+// g, u: n bf16 bit patterns each; r, q: n floats.  n < 2^31.
+extern "C" int fp8rl_probe_silu_fast(const uint16_t* g, const uint16_t* u, float* r, float* q, long long n,
+                                     void* stream) {
+  if (n < 0 || n >= (1ll << 31)) return 1;
+  if (n == 0) return 0;
+  hipLaunchKernelGGL(silu_fast_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), g, u, r, q, (int64_t)n);
+  return hipGetLastError() == hipSuccess ? 0 : 4;
 }

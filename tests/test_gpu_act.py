@@ -112,6 +112,44 @@ def test_silu_mul_exhaustive_pairs(fp8rl, exponent):
     check_fused(gu, gu.shape[1] // 2, q, s, h, big=True)
 
 
+def test_silu_fast_path_error_bound(fp8rl):
+    """The premise of the kernel's fast path: wherever it is taken (|q| >= 2^-100, r
+    finite), its fp32 result is within 10 fp32 ulps (the stated error bound) of the
+    exact SiLU(g) * u, inside the 12-ulp guard around the bf16 half-way point.
+    Measured for every gate bit pattern and up significand (relative error does not
+    depend on up's exponent)."""
+    import ctypes
+    import os
+    announce("silu fast-path error bound, 2^24 pairs")
+    lib = ctypes.CDLL(os.path.join(os.path.dirname(fp8rl.LIB_PATH), "libfp8rl_probe.so"))
+    fn = lib.fp8rl_probe_silu_fast
+    fn.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_longlong, ctypes.c_void_p]
+    i = np.arange(1 << 24, dtype=np.int64)
+    gb = (i & 0xFFFF).astype(np.uint16)
+    ub = (0x3F80 | (i >> 16 & 0x7F) | ((i >> 23) << 15)).astype(np.uint16)
+    g_t = torch.from_numpy(gb.view(np.int16)).cuda()
+    u_t = torch.from_numpy(ub.view(np.int16)).cuda()
+    r_t = torch.empty(i.size, dtype=torch.float32, device="cuda")
+    q_t = torch.empty_like(r_t)
+    assert fn(g_t.data_ptr(), u_t.data_ptr(), r_t.data_ptr(), q_t.data_ptr(), i.size,
+              torch.cuda.current_stream().cuda_stream) == 0
+    torch.cuda.synchronize()
+    r = r_t.cpu().numpy().astype(np.float64)
+    q = q_t.cpu().numpy().astype(np.float64)
+    with np.errstate(all="ignore"):
+        g = quant.bf16_bits_to_f32(gb).astype(np.float64)
+        u = quant.bf16_bits_to_f32(ub).astype(np.float64)
+        x = g / (1.0 + np.exp(-g)) * u
+        taken = (np.abs(q) >= 2.0 ** -100) & (np.abs(r) <= np.finfo(np.float32).max)
+        _, e = np.frexp(np.abs(r[taken]))
+        ulp = np.ldexp(1.0, np.maximum(e - 1, -126) - 23)
+        err = np.abs(r[taken] - x[taken]) / ulp
+    assert taken.mean() > 0.5
+    sys_max = float(err.max())
+    print(f"fast path taken for {taken.mean():.4f} of pairs; max error {sys_max:.3f} ulp")
+    assert sys_max <= 10.0, sys_max
+
+
 def test_silu_mul_quant_dense_mlp_full_sampled(fp8rl):
     """Full Qwen3-8B MLP shape (8192 tokens, intermediate 12288): the whole step runs
     on the GPU, the oracle checks 256 seeded rows (the step is row-independent)."""
