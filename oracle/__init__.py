@@ -17,6 +17,8 @@ This package is a plain, slow, obviously-correct restatement of what the paper
   then 1x128 group quantisation (section 2.1.1: down_proj / fc2 are quantised
   like every linear, activations dynamically), and the row gather of quantised
   activations that MoE dispatch needs.
+* ``ue8m0`` -- the power-of-two (UE8M0) scale variant of both quantisers
+  (section 2.4.3 "Scaling Factor: FP32 vs Power-of-2").
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import, call or execute anything in this package.  The HIP
@@ -24,4 +26,4 @@ product path never does; it shares no code, table or constant generator with
 this package.  Everything here is numpy on the CPU (plus one small C file,
 ``e4m3_sweep.c``, used only by the exhaustive element-map test).
 """
-from . import e4m3, quant, gemm, act  # noqa: F401
+from . import e4m3, quant, gemm, act, ue8m0  # noqa: F401
