@@ -19,7 +19,7 @@ FP8 MFMA loop with its clock.
 `cpu_baseline` times the CPU oracle on a bounded row sample of the same step.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload prefill|requant|moe|decode|mlp|moe_block|copy]
+                       [--workload prefill|requant|moe|decode|mlp|moe_block|ue8m0|copy]
                        [--no-cpu-baseline] [--no-extra]
 """
 import argparse
@@ -46,7 +46,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe", "copy", "mlp",
-                                                              "moe_block"])
+                                                              "moe_block", "ue8m0"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -154,6 +154,39 @@ def prefill(args, fp8rl):
         },
     }
     return out, (a, w)
+
+
+def prefill_ue8m0(args, fp8rl, steps=10, warmup=3):
+    """The same prefill step with power-of-two (UE8M0) scales: both quantisers in
+    their power-of-two form and the GEMM on the MX-scaled MFMA (section 2.4.3)."""
+    m, k, n = 8192, 4096, 24576
+    a, w = synth.prefill_linear(seed=args.seed, device="cuda", m=m, k=k, n=n)
+    qw = torch.empty((n, k), dtype=torch.uint8, device="cuda")
+    sw = torch.empty((n // 128, k // 128), dtype=torch.float32, device="cuda")
+    qa = torch.empty((m, k), dtype=torch.uint8, device="cuda")
+    sa = torch.empty((k // 128, m), dtype=torch.float32, device="cuda")
+    y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+    timer = KernelTimer()
+
+    def step():
+        with timer.span("quant_weight"):
+            fp8rl.fp8rl_quant_weight_block128_ue8m0(w, q=qw, scale=sw)
+        with timer.span("quant_act"):
+            fp8rl.fp8rl_quant_act_token_group128_ue8m0(a, q=qa, scale=sa)
+        with timer.span("gemm"):
+            fp8rl.fp8rl_gemm_w8a8_block_ue8m0(qa, sa, qw, sw, y=y)
+
+    ms, _ = timed_loop(step, steps, warmup, timer)
+    kern = timer.averages_ms()
+    flops = 2.0 * m * n * k
+    t = flops / (kern["gemm"] * 1e-3) / 1e12
+    res = {"workload": "Qwen3-8B prefill gate_up linear with power-of-two (UE8M0) scales: requant + quant + "
+                       "GEMM on the MX-scaled MFMA", "ms_per_step": round(ms, 4),
+           "kernels_ms": {kk: round(v, 5) for kk, v in kern.items()},
+           "gemm_TFLOP/s": round(t, 1), "gemm_frac_fp8_peak": round(t / FP8_PEAK_TFLOPS, 4)}
+    del a, w, qw, qa, y
+    torch.cuda.empty_cache()
+    return res
 
 
 # ---------------------------------------------------------------------------
@@ -568,7 +601,8 @@ def main():
             print(json.dumps({"workload": "device-to-device copy of 4 GiB (torch copy_)",
                               "GB/s": hbm_copy_reference()}), flush=True)
             return
-        fn = {"requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block}[args.workload]
+        fn = {"requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block,
+              "ue8m0": prefill_ue8m0}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
     out, (a, w) = prefill(args, fp8rl)
@@ -576,7 +610,8 @@ def main():
                 "scaling": "weak", "vs_baseline": None, "data": "synthetic"})
     if not args.no_extra:
         extra = {"weight_resync": requant(args, fp8rl), "moe_grouped": moe(args, fp8rl),
-                 "decode_36_layers": decode(args, fp8rl), "dense_mlp": mlp(args, fp8rl),
+                 "decode_36_layers": decode(args, fp8rl), "prefill_ue8m0": prefill_ue8m0(args, fp8rl),
+                 "dense_mlp": mlp(args, fp8rl),
                  "moe_block": moe_block(args, fp8rl), "hbm_copy_GB/s": hbm_copy_reference(),
                  "mfma_probe": mfma_probe()}
         out["extra"] = extra

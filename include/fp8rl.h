@@ -168,6 +168,42 @@ int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld
                                   void* stream);
 
 /*
+ * Power-of-two (UE8M0) scale variant (section 2.4.3, "Scaling Factor: FP32 vs
+ * Power-of-2": the same 128x128 / 1x128 blocks with scales restricted to 2^k).
+ * Same arguments, layouts, error codes and alignment rules as the fp32-scale
+ * entry points above; the scales are written as fp32 values 2^k:
+ *   k = the smallest integer with amax <= 448 * 2^k, clamped below at -127
+ *       (the smallest UE8M0 value); 1.0 for an all-zero block or group;
+ *   code = E4M3(x * 2^-k) (an exact scaling, then round to nearest even).
+ * The UE8M0 byte of a scale is k + 127, the fp32 value's exponent field.
+ */
+int fp8rl_quant_weight_block128_ue8m0(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
+                                      uint8_t* q, int64_t ldq, float* scale, void* stream);
+
+int fp8rl_quant_act_token_group128_ue8m0(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
+                                         uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
+                                         void* stream);
+
+/*
+ * The dense and grouped GEMMs for power-of-two scales: the same products as
+ * fp8rl_gemm_w8a8_block / fp8rl_grouped_gemm_w8a8_block, with the scales
+ * applied by gfx950's MX-scaled MFMA (no per-K-block scale arithmetic in the
+ * kernel).  Same arguments, layouts, error codes and alignment rules.
+ * Precondition (not checked, it would need a device read): every sa and sw
+ * entry is a power of two 2^-127 .. 2^127, as the _ue8m0 quantisers write
+ * them; only the exponent field of each scale is read.
+ */
+int fp8rl_gemm_w8a8_block_ue8m0(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                const uint8_t* qw, int64_t ldw, const float* sw,
+                                uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k, void* stream);
+
+int fp8rl_grouped_gemm_w8a8_block_ue8m0(const uint8_t* qa, const float* sa, int64_t ld_sa,
+                                        const uint8_t* qw, const float* sw,
+                                        const int32_t* group_offsets, int64_t num_groups,
+                                        int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
+                                        void* stream);
+
+/*
  * Down-projection input of the gated MLP, quantised (section 2.1.1: down_proj /
  * MoE fc2 are quantised like every linear layer, their activations dynamically
  * with 1x128 groups; section 3.1).  From the fused gate_up output:

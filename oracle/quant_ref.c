@@ -12,6 +12,10 @@
  *   code  = E4M3(fl32(x / scale)), round to nearest even on the E4M3 grid,
  *           saturating at 448, sign of x kept.
  *
+ * The power-of-two (UE8M0) variant (section 2.4.3) replaces the scale by 2^k,
+ * k the smallest integer with amax <= 448 * 2^k (clamped at -127; 1.0 for
+ * amax == 0), and the quotient by the exact product x * 2^-k.
+ *
  * Build: gcc -O2 -fopenmp -ffp-contract=off -fno-fast-math -shared -fPIC
  * (no flag that changes IEEE behaviour; x86-64 SSE keeps subnormals).
  */
@@ -107,5 +111,57 @@ void oracle_e4m3_of_quotient(const uint16_t* x, const uint16_t* amax, int64_t co
         float s = scale_of(fabsf(bf16_to_f32(amax[i])));
         volatile float quot = bf16_to_f32(x[i]) / s;
         out[i] = e4m3_encode(quot);
+    }
+}
+
+/* Power-of-two scale: 2^k with k the smallest integer such that amax <= 448 * 2^k
+ * (every comparison exact in double), clamped at 2^-127; 1.0 for amax == 0. */
+static int pow2_k(float amax) {
+    if (amax == 0.0f) return 0;
+    int k = (int)ceil(log2((double)amax / 448.0));
+    while ((double)amax > 448.0 * ldexp(1.0, k)) ++k;
+    while ((double)amax <= 448.0 * ldexp(1.0, k - 1)) --k;
+    return k < -127 ? -127 : k;
+}
+
+static uint8_t e4m3_pow2(float x, int k) {
+    return e4m3_encode((float)ldexp((double)x, -k));   /* exact above 2^-126; below, E4M3 gives +-0 */
+}
+
+void oracle_quant_weight_block128_ue8m0(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
+                                        uint8_t* q, int64_t ldq, float* scale) {
+    int64_t nbn = n / 128, nbk = k / 128;
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t b = 0; b < nbn * nbk; ++b) {
+        int64_t bi = b / nbk, bj = b % nbk;
+        float amax = 0.0f;
+        for (int64_t r = 0; r < 128; ++r)
+            for (int64_t c = 0; c < 128; ++c) {
+                float x = fabsf(bf16_to_f32(w[(bi * 128 + r) * ldw + bj * 128 + c]));
+                if (x > amax) amax = x;
+            }
+        int e = pow2_k(amax);
+        scale[bi * nbk + bj] = ldexpf(1.0f, e);
+        for (int64_t r = 0; r < 128; ++r)
+            for (int64_t c = 0; c < 128; ++c)
+                q[(bi * 128 + r) * ldq + bj * 128 + c] = e4m3_pow2(bf16_to_f32(w[(bi * 128 + r) * ldw + bj * 128 + c]), e);
+    }
+}
+
+void oracle_quant_act_token_group128_ue8m0(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
+                                           uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale) {
+    int64_t ng = k / 128;
+    #pragma omp parallel for schedule(dynamic, 64)
+    for (int64_t t = 0; t < m * ng; ++t) {
+        int64_t row = t / ng, g = t % ng;
+        const uint16_t* src = a + row * lda + g * 128;
+        float amax = 0.0f;
+        for (int c = 0; c < 128; ++c) {
+            float x = fabsf(bf16_to_f32(src[c]));
+            if (x > amax) amax = x;
+        }
+        int e = pow2_k(amax);
+        scale[g * ld_scale + row] = ldexpf(1.0f, e);
+        for (int c = 0; c < 128; ++c) q[row * ldq + g * 128 + c] = e4m3_pow2(bf16_to_f32(src[c]), e);
     }
 }

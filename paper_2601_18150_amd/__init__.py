@@ -24,6 +24,8 @@ __all__ = [
     "fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
     "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
     "fp8rl_gemm_w8a8_block_workspace_size", "fp8rl_gemm_w8a8_block_ws",
+    "fp8rl_quant_weight_block128_ue8m0", "fp8rl_quant_act_token_group128_ue8m0",
+    "fp8rl_gemm_w8a8_block_ue8m0", "fp8rl_grouped_gemm_w8a8_block_ue8m0",
     "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8",
     "fp8rl_status_string", "fp8rl_version",
     "quant_weight_block128", "quant_act_token_group128", "gemm_w8a8_block",
@@ -63,6 +65,10 @@ def _load():
         "fp8rl_gemm_w8a8_block": [P, I, P, I, P, I, P, P, I, I, I, I, P],
         "fp8rl_grouped_gemm_w8a8_block": [P, P, I, P, P, P, I, I, P, I, I, P],
         "fp8rl_gemm_w8a8_block_ws": [P, I, P, I, P, I, P, P, I, I, I, I, P, I, P],
+        "fp8rl_quant_weight_block128_ue8m0": [P, I, I, I, P, I, P, P],
+        "fp8rl_quant_act_token_group128_ue8m0": [P, I, I, I, P, I, P, I, P],
+        "fp8rl_gemm_w8a8_block_ue8m0": [P, I, P, I, P, I, P, P, I, I, I, I, P],
+        "fp8rl_grouped_gemm_w8a8_block_ue8m0": [P, P, I, P, P, P, I, I, P, I, I, P],
         "fp8rl_silu_mul_quant_group128": [P, I, I, I, P, I, P, I, P, I, P],
         "fp8rl_gather_rows_fp8": [P, I, P, I, I, P, I, I, P, I, P, I, P],
     }
@@ -146,6 +152,16 @@ def fp8rl_version() -> int:
 def fp8rl_quant_weight_block128(w: torch.Tensor, q: torch.Tensor | None = None,
                                 scale: torch.Tensor | None = None, stream=None):
     """bf16 weight [N][K] -> (E4M3 codes uint8 [N][K], fp32 scales [N/128][K/128])."""
+    return _quant_weight("fp8rl_quant_weight_block128", w, q, scale, stream)
+
+
+def fp8rl_quant_weight_block128_ue8m0(w: torch.Tensor, q: torch.Tensor | None = None,
+                                      scale: torch.Tensor | None = None, stream=None):
+    """As fp8rl_quant_weight_block128 with power-of-two (UE8M0) scales 2^k, stored as fp32."""
+    return _quant_weight("fp8rl_quant_weight_block128_ue8m0", w, q, scale, stream)
+
+
+def _quant_weight(name, w, q, scale, stream):
     if w.dtype != torch.bfloat16 or w.dim() != 2:
         raise TypeError("w must be a 2-D bfloat16 tensor")
     n, k = w.shape
@@ -157,9 +173,8 @@ def fp8rl_quant_weight_block128(w: torch.Tensor, q: torch.Tensor | None = None,
     _dev(w, q, scale)
     if scale.dtype != torch.float32 or not scale.is_contiguous() or scale.numel() < (n // 128) * (k // 128):
         raise ValueError("scale must be a contiguous fp32 tensor of [N/128][K/128] elements")
-    st = load().fp8rl_quant_weight_block128(w.data_ptr(), n, k, _ld(w), q.data_ptr(), _ld(q),
-                                         scale.data_ptr(), _stream(stream))
-    _check("fp8rl_quant_weight_block128", st)
+    st = getattr(load(), name)(w.data_ptr(), n, k, _ld(w), q.data_ptr(), _ld(q), scale.data_ptr(), _stream(stream))
+    _check(name, st)
     return q, scale
 
 
@@ -167,6 +182,17 @@ def fp8rl_quant_act_token_group128(a: torch.Tensor, q: torch.Tensor | None = Non
                                    scale: torch.Tensor | None = None, ld_scale: int | None = None,
                                    stream=None):
     """bf16 activations [M][K] -> (E4M3 codes uint8 [M][K], fp32 scales [K/128][ld_scale])."""
+    return _quant_act("fp8rl_quant_act_token_group128", a, q, scale, ld_scale, stream)
+
+
+def fp8rl_quant_act_token_group128_ue8m0(a: torch.Tensor, q: torch.Tensor | None = None,
+                                         scale: torch.Tensor | None = None, ld_scale: int | None = None,
+                                         stream=None):
+    """As fp8rl_quant_act_token_group128 with power-of-two (UE8M0) scales 2^k, stored as fp32."""
+    return _quant_act("fp8rl_quant_act_token_group128_ue8m0", a, q, scale, ld_scale, stream)
+
+
+def _quant_act(name, a, q, scale, ld_scale, stream):
     if a.dtype != torch.bfloat16 or a.dim() != 2:
         raise TypeError("a must be a 2-D bfloat16 tensor")
     m, k = a.shape
@@ -182,9 +208,9 @@ def fp8rl_quant_act_token_group128(a: torch.Tensor, q: torch.Tensor | None = Non
     _dev(a, q, scale)
     if scale.dtype != torch.float32 or scale.numel() < (k // 128) * ld_scale and m > 0:
         raise ValueError("scale must be fp32 with at least [K/128][ld_scale] elements")
-    st = load().fp8rl_quant_act_token_group128(a.data_ptr(), m, k, _ld(a) if m else k, q.data_ptr(),
-                                            _ld(q) if m else k, scale.data_ptr(), ld_scale, _stream(stream))
-    _check("fp8rl_quant_act_token_group128", st)
+    st = getattr(load(), name)(a.data_ptr(), m, k, _ld(a) if m else k, q.data_ptr(), _ld(q) if m else k,
+                               scale.data_ptr(), ld_scale, _stream(stream))
+    _check(name, st)
     return q, scale
 
 
@@ -212,12 +238,23 @@ def fp8rl_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, 
                           y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """y[M][N] bf16 = blockwise-scaled FP8 product of qa [M][K] (scales sa [K/128][>=M])
     and qw [N][K] (scales sw [N/128][K/128])."""
+    return _gemm("fp8rl_gemm_w8a8_block", qa, sa, qw, sw, y, stream)
+
+
+def fp8rl_gemm_w8a8_block_ue8m0(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
+                                y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """As fp8rl_gemm_w8a8_block for power-of-two scales (from the _ue8m0 quantisers), which the
+    MX-scaled MFMA applies in hardware."""
+    return _gemm("fp8rl_gemm_w8a8_block_ue8m0", qa, sa, qw, sw, y, stream)
+
+
+def _gemm(name, qa, sa, qw, sw, y, stream):
     qa, qw, y, m, n, k = _dense_args(qa, sa, qw, sw, y)
     if m == 0:
         return y
-    st = load().fp8rl_gemm_w8a8_block(qa.data_ptr(), _ld(qa), sa.data_ptr(), sa.stride(0), qw.data_ptr(),
-                                   _ld(qw), sw.data_ptr(), y.data_ptr(), _ld(y), m, n, k, _stream(stream))
-    _check("fp8rl_gemm_w8a8_block", st)
+    st = getattr(load(), name)(qa.data_ptr(), _ld(qa), sa.data_ptr(), sa.stride(0), qw.data_ptr(), _ld(qw),
+                               sw.data_ptr(), y.data_ptr(), _ld(y), m, n, k, _stream(stream))
+    _check(name, st)
     return y
 
 
@@ -252,6 +289,17 @@ def fp8rl_grouped_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.
     qa [R][K] codes grouped by expert; sa [K/128][ld >= R]; qw [G][N][K];
     sw [G][N/128][K/128]; group_offsets int32 [G+1] on the device.
     """
+    return _grouped("fp8rl_grouped_gemm_w8a8_block", qa, sa, qw, sw, group_offsets, y, stream)
+
+
+def fp8rl_grouped_gemm_w8a8_block_ue8m0(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
+                                        group_offsets: torch.Tensor, y: torch.Tensor | None = None,
+                                        stream=None) -> torch.Tensor:
+    """As fp8rl_grouped_gemm_w8a8_block for power-of-two scales (MX-scaled MFMA)."""
+    return _grouped("fp8rl_grouped_gemm_w8a8_block_ue8m0", qa, sa, qw, sw, group_offsets, y, stream)
+
+
+def _grouped(name, qa, sa, qw, sw, group_offsets, y, stream):
     qa, qw = _u8(qa), _u8(qw)
     r, k = qa.shape
     g, n, k2 = qw.shape
@@ -272,10 +320,9 @@ def fp8rl_grouped_gemm_w8a8_block(qa: torch.Tensor, sa: torch.Tensor, qw: torch.
     _dev(qa, sa, qw, sw, group_offsets, y)
     if r == 0:
         return y
-    st = load().fp8rl_grouped_gemm_w8a8_block(qa.data_ptr(), sa.data_ptr(), sa.stride(0), qw.data_ptr(),
-                                           sw.data_ptr(), group_offsets.data_ptr(), g, r, y.data_ptr(),
-                                           n, k, _stream(stream))
-    _check("fp8rl_grouped_gemm_w8a8_block", st)
+    st = getattr(load(), name)(qa.data_ptr(), sa.data_ptr(), sa.stride(0), qw.data_ptr(), sw.data_ptr(),
+                               group_offsets.data_ptr(), g, r, y.data_ptr(), n, k, _stream(stream))
+    _check(name, st)
     return y
 
 

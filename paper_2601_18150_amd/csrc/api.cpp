@@ -54,8 +54,8 @@ const char* fp8rl_status_string(int status) {
 
 int fp8rl_version(void) { return 100; }   // 0.1.0
 
-int fp8rl_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q,
-                                int64_t ldq, float* scale, void* stream) {
+static int quant_weight(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q, int64_t ldq,
+                        float* scale, void* stream, bool pow2) {
   if (n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
   if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (n >= kMaxDim || k >= kMaxDim || (n / 128) * (k / 128) >= (int64_t(1) << 24))
@@ -65,11 +65,21 @@ int fp8rl_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t
   if (ldw < k || ldq < k) return FP8RL_ERR_INVALID_ARG;
   if (!aligned(w, 16) || !aligned(q, 16) || !aligned(scale, 4) || ldw % 8 || ldq % 16)
     return FP8RL_ERR_MISALIGNED;
-  return hip_status(fp8rl::launch_quant_weight_block128(w, n, k, ldw, q, ldq, scale, as_stream(stream)));
+  return hip_status(fp8rl::launch_quant_weight_block128(w, n, k, ldw, q, ldq, scale, as_stream(stream), pow2));
 }
 
-int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda, uint8_t* q,
-                                   int64_t ldq, float* scale, int64_t ld_scale, void* stream) {
+int fp8rl_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q,
+                                int64_t ldq, float* scale, void* stream) {
+  return quant_weight(w, n, k, ldw, q, ldq, scale, stream, false);
+}
+
+int fp8rl_quant_weight_block128_ue8m0(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q,
+                                      int64_t ldq, float* scale, void* stream) {
+  return quant_weight(w, n, k, ldw, q, ldq, scale, stream, true);
+}
+
+static int quant_act(const uint16_t* a, int64_t m, int64_t k, int64_t lda, uint8_t* q, int64_t ldq, float* scale,
+                     int64_t ld_scale, void* stream, bool pow2) {
   if (m < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
   if (k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (m >= kMaxDim || k >= kMaxDim || m * (k / 128) >= (int64_t(1) << 28)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
@@ -79,7 +89,17 @@ int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int6
   if (!aligned(a, 16) || !aligned(q, 16) || !aligned(scale, 4) || lda % 8 || ldq % 16)
     return FP8RL_ERR_MISALIGNED;
   return hip_status(
-      fp8rl::launch_quant_act_token_group128(a, m, k, lda, q, ldq, scale, ld_scale, as_stream(stream)));
+      fp8rl::launch_quant_act_token_group128(a, m, k, lda, q, ldq, scale, ld_scale, as_stream(stream), pow2));
+}
+
+int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda, uint8_t* q,
+                                   int64_t ldq, float* scale, int64_t ld_scale, void* stream) {
+  return quant_act(a, m, k, lda, q, ldq, scale, ld_scale, stream, false);
+}
+
+int fp8rl_quant_act_token_group128_ue8m0(const uint16_t* a, int64_t m, int64_t k, int64_t lda, uint8_t* q,
+                                         int64_t ldq, float* scale, int64_t ld_scale, void* stream) {
+  return quant_act(a, m, k, lda, q, ldq, scale, ld_scale, stream, true);
 }
 
 int fp8rl_silu_mul_quant_group128(const uint16_t* gu, int64_t m, int64_t inter, int64_t ld_gu, uint8_t* q,
@@ -121,7 +141,16 @@ int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64
   const int st = check_dense(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k);
   if (st != kLaunch) return st;
   return hip_status(
-      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream)));
+      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream), false));
+}
+
+int fp8rl_gemm_w8a8_block_ue8m0(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y, int64_t ldy,
+                                int64_t m, int64_t n, int64_t k, void* stream) {
+  const int st = check_dense(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k);
+  if (st != kLaunch) return st;
+  return hip_status(
+      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream), true));
 }
 
 int64_t fp8rl_gemm_w8a8_block_workspace_size(int64_t m, int64_t n, int64_t k) {
@@ -143,12 +172,28 @@ int fp8rl_gemm_w8a8_block_ws(const uint8_t* qa, int64_t lda, const float* sa, in
                                                            static_cast<float*>(workspace), splits,
                                                            as_stream(stream)));
   return hip_status(
-      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream)));
+      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream), false));
 }
+
+static int grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw, const float* sw,
+                   const int32_t* group_offsets, int64_t num_groups, int64_t total_rows, uint16_t* y, int64_t n,
+                   int64_t k, void* stream, bool pow2);
 
 int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw,
                                   const float* sw, const int32_t* group_offsets, int64_t num_groups,
                                   int64_t total_rows, uint16_t* y, int64_t n, int64_t k, void* stream) {
+  return grouped(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k, stream, false);
+}
+
+int fp8rl_grouped_gemm_w8a8_block_ue8m0(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw,
+                                        const float* sw, const int32_t* group_offsets, int64_t num_groups,
+                                        int64_t total_rows, uint16_t* y, int64_t n, int64_t k, void* stream) {
+  return grouped(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k, stream, true);
+}
+
+static int grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw, const float* sw,
+                   const int32_t* group_offsets, int64_t num_groups, int64_t total_rows, uint16_t* y, int64_t n,
+                   int64_t k, void* stream, bool pow2) {
   if (total_rows < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
   if (num_groups < 1) return FP8RL_ERR_INVALID_ARG;
   if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
@@ -163,7 +208,7 @@ int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld
       !aligned(group_offsets, 4))
     return FP8RL_ERR_MISALIGNED;
   return hip_status(fp8rl::launch_grouped_gemm_w8a8_block(qa, sa, ld_sa, qw, sw, group_offsets, num_groups,
-                                                          total_rows, y, n, k, as_stream(stream)));
+                                                          total_rows, y, n, k, as_stream(stream), pow2));
 }
 
 }  // extern "C"

@@ -90,14 +90,16 @@ struct OneJob {
   }
 };
 
-template <class C>
+// kMx: power-of-two scales through the MX-scaled MFMA (gemm_core.hpp).
+template <class C, bool kMx>
 __global__ __launch_bounds__(C::kThreads) void gemm_w8a8_block_kernel(
     const uint8_t* __restrict__ qa, int64_t lda, const float* __restrict__ sa, int64_t ld_sa,
     const uint8_t* __restrict__ qw, int64_t ldw, const float* __restrict__ sw,
     uint16_t* __restrict__ y, int64_t ldy, int64_t M, int64_t N, int KB, int tiles_m, int tiles_n) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes];
   DenseJobs<C> jobs{(int)blockIdx.x, (int)gridDim.x, tiles_m, tiles_n, (int)M};
-  gemm_tiles<C, false, kCrossTiles<C>>(qa, lda, sa, ld_sa, qw, ldw, sw, KB, y, ldy, nullptr, (int)N, KB, jobs, lds);
+  gemm_tiles<C, false, kCrossTiles<C>, DenseJobs<C>, kMx>(qa, lda, sa, ld_sa, qw, ldw, sw, KB, y, ldy, nullptr,
+                                                          (int)N, KB, jobs, lds);
 }
 
 // Split-K dense GEMM, for shapes whose tiles alone cannot fill the GPU (decode:
@@ -201,7 +203,7 @@ struct GroupedJobs {
   }
 };
 
-template <class C>
+template <class C, bool kMx>
 __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
     const uint8_t* __restrict__ qa, const float* __restrict__ sa, int64_t ld_sa,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw,
@@ -236,7 +238,8 @@ __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
   GroupedJobs<C> jobs{(int)blockIdx.x, (int)gridDim.x, __builtin_amdgcn_readfirstlane(tstart[G]), tiles_n, G,
                       tstart, rstart, N, K};
   const int KB = (int)(K / 128);
-  gemm_tiles<C, false, kCrossTiles<C>>(qa, K, sa, ld_sa, qw, K, sw, KB, y, N, nullptr, (int)N, KB, jobs, lds);
+  gemm_tiles<C, false, kCrossTiles<C>, GroupedJobs<C>, kMx>(qa, K, sa, ld_sa, qw, K, sw, KB, y, N, nullptr, (int)N,
+                                                            KB, jobs, lds);
 }
 
 // Workgroups that stay resident on one CU for a configuration (LDS-limited).
@@ -245,7 +248,7 @@ constexpr int per_cu() { return (160 * 1024) / (C::kLdsBytes + kExtraLds); }
 
 constexpr int kCus = 256;     // MI355X; grids of kCus * per_cu() are multiples of 8 (one per XCD)
 
-template <class C>
+template <class C, bool kMx>
 hipError_t launch_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
                         int64_t ldw, const float* sw, uint16_t* y, int64_t ldy, int64_t m, int64_t n,
                         int64_t k, hipStream_t stream) {
@@ -255,13 +258,13 @@ hipError_t launch_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t
   // persistent grid with the cross-tile pipeline, else one workgroup per tile
   // (a persistent grid without it measured no faster)
   const int64_t slots = kCrossTiles<C> ? (int64_t)kCus * per_cu<C>() : total;
-  hipLaunchKernelGGL(gemm_w8a8_block_kernel<C>, dim3((unsigned)(total < slots ? total : slots)),
+  hipLaunchKernelGGL((gemm_w8a8_block_kernel<C, kMx>), dim3((unsigned)(total < slots ? total : slots)),
                      dim3(C::kThreads), 0, stream, qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n,
                      (int)(k / 128), tiles_m, tiles_n);
   return hipGetLastError();
 }
 
-template <class C>
+template <class C, bool kMx>
 hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw,
                           const float* sw, const int32_t* offsets, int64_t g, int64_t rows, uint16_t* y,
                           int64_t n, int64_t k, hipStream_t stream) {
@@ -270,7 +273,7 @@ hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, con
   const int64_t total = max_tiles_m * tiles_n;
   // persistent grid with the cross-tile pipeline, else one workgroup per tile
   const int64_t slots = kCrossTiles<C> ? (int64_t)kCus * per_cu<C, 2 * 4 * (kMaxExperts + 1)>() : total;
-  hipLaunchKernelGGL(grouped_gemm_w8a8_block_kernel<C>, dim3((unsigned)(total < slots ? total : slots)),
+  hipLaunchKernelGGL((grouped_gemm_w8a8_block_kernel<C, kMx>), dim3((unsigned)(total < slots ? total : slots)),
                      dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw, sw, offsets, (int)g, y, n, k,
                      (int)tiles_n);
   return hipGetLastError();
@@ -280,10 +283,13 @@ hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, con
 
 hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
                                   const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y, int64_t ldy,
-                                  int64_t m, int64_t n, int64_t k, hipStream_t stream) {
-  if (m >= 2048 && n >= 2048)
-    return launch_dense<CfgLarge>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
-  return launch_dense<CfgSmall>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+                                  int64_t m, int64_t n, int64_t k, hipStream_t stream, bool pow2_scales) {
+  const bool large = m >= 2048 && n >= 2048;
+  if (pow2_scales)
+    return large ? launch_dense<CfgLarge, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+                 : launch_dense<CfgSmall, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+  return large ? launch_dense<CfgLarge, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+               : launch_dense<CfgSmall, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
 }
 
 int splitk_factor(int64_t m, int64_t n, int64_t k) {
@@ -324,9 +330,12 @@ hipError_t launch_gemm_w8a8_block_splitk(const uint8_t* qa, int64_t lda, const f
 hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,
                                           const uint8_t* qw, const float* sw, const int32_t* group_offsets,
                                           int64_t num_groups, int64_t total_rows, uint16_t* y, int64_t n,
-                                          int64_t k, hipStream_t stream) {
-  return launch_grouped<CfgSmall>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
-                                  stream);
+                                          int64_t k, hipStream_t stream, bool pow2_scales) {
+  if (pow2_scales)
+    return launch_grouped<CfgSmall, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
+                                          stream);
+  return launch_grouped<CfgSmall, false>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
+                                         stream);
 }
 
 }  // namespace fp8rl

@@ -12,6 +12,9 @@
 // accumulator with one FMA by the combined scale sA[m, kb] * sW[nb, kb]:
 //     acc += P_kb * (sA * sW)
 // i.e. the per-K-block scale is applied in the epilogue of each K step.
+// With power-of-two (UE8M0) scales (section 2.4.3) the MX-scaled form of the
+// same instruction applies 2^(eA + eW) to the products itself and accumulates
+// straight into acc: no per-step scale arithmetic (kMx).
 //
 // Data movement per K step: the block's W and A tiles (BN x 128 and BM x 128
 // bytes) go straight from global memory into an LDS ring (global_load_lds,
@@ -171,7 +174,7 @@ struct TileJob {
 // the only vector-memory traffic of the loop, so the one explicit vmcnt wait
 // per step is the only wait on global memory (at a tile's first step it also
 // covers the previous tile's output stores).
-template <class C, bool kPartial, bool kCross, class Jobs>
+template <class C, bool kPartial, bool kCross, class Jobs, bool kMx = false>
 __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64_t lda,
                                            const float* __restrict__ sa, int64_t ld_sa,
                                            const uint8_t* __restrict__ qw, int64_t ldw,
@@ -279,10 +282,20 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       constexpr int kDmaSpread = C::TN >= 8 ? C::TN / 2 : 1;   // sub-tile rows that carry DMA issue
       const uint8_t* st = lds + slot * C::kStageBytes;
       const float* sts = reinterpret_cast<const float*>(st + C::kWBytes + C::kABytes) + wm * C::WTM + (lane & 15);
-      const float swv = swrow[kb];
       float sc[C::TM];
+      int se[C::TM];
+      int sw_e8 = 0;
+      if constexpr (kMx) {
+        // power-of-two scales: their UE8M0 bytes (the fp32 exponent fields) go
+        // to the MX-scaled MFMA, which applies them to the products itself
+        sw_e8 = (int)(__float_as_uint(swrow[kb]) >> 23);
 #pragma unroll
-      for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sts[tm * 16] * swv;
+        for (int tm = 0; tm < C::TM; ++tm) se[tm] = (int)(__float_as_uint(sts[tm * 16]) >> 23);
+      } else {
+        const float swv = swrow[kb];
+#pragma unroll
+        for (int tm = 0; tm < C::TM; ++tm) sc[tm] = sts[tm * 16] * swv;
+      }
 
       const uint8_t* sta = st + C::kWBytes + wm * C::WTM * 128;
       const uint8_t* stw = st + wn * C::WTN * 128;
@@ -308,15 +321,25 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
         if (tn == 0 && sdma && refill) lds_dma4(dsa, dslot + C::kWBytes + C::kABytes + wave * 256);
         v8i32 af_next = af;
         if (tn + 1 < C::TN) af_next = lds_frag2(stw + (tn + 1) * 16 * 128, f0, f1);
-        // all MFMAs of the sub-tile row first (independent results in flight),
-        // then their scale FMAs
-        v4f32 p[C::TM];
+        if constexpr (kMx) {
+          // lane L supplies the scale of its own operand rows: weight row L % 16
+          // (one 128-row block per wave: the uniform sw_e8) and token L % 16 of
+          // the sub-tile (se), for all four 32-wide K slices of the block
 #pragma unroll
-        for (int tm = 0; tm < C::TM; ++tm) p[tm] = mfma_fp8_16x16x128(af, bf[tm]);
+          for (int tm = 0; tm < C::TM; ++tm)
+            acc[tn][tm] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf[tm], acc[tn][tm], 0, 0, 0, sw_e8,
+                                                                           0, se[tm]);
+        } else {
+          // all MFMAs of the sub-tile row first (independent results in flight),
+          // then their scale FMAs
+          v4f32 p[C::TM];
 #pragma unroll
-        for (int tm = 0; tm < C::TM; ++tm)
+          for (int tm = 0; tm < C::TM; ++tm) p[tm] = mfma_fp8_16x16x128(af, bf[tm]);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[tn][tm][r] = __builtin_fmaf(p[tm][r], sc[tm], acc[tn][tm][r]);
+          for (int tm = 0; tm < C::TM; ++tm)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[tn][tm][r] = __builtin_fmaf(p[tm][r], sc[tm], acc[tn][tm][r]);
+        }
         af = af_next;
       }
       slot ^= 1;

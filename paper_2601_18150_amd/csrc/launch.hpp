@@ -8,12 +8,14 @@
 
 namespace fp8rl {
 
+// pow2_scale: power-of-two (UE8M0) block scales instead of fl32(amax / 448)
 hipError_t launch_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
-                                        uint8_t* q, int64_t ldq, float* scale, hipStream_t stream);
+                                        uint8_t* q, int64_t ldq, float* scale, hipStream_t stream,
+                                        bool pow2_scale);
 
 hipError_t launch_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
                                            uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
-                                           hipStream_t stream);
+                                           hipStream_t stream, bool pow2_scale);
 
 hipError_t launch_silu_mul_quant_group128(const uint16_t* gu, int64_t m, int64_t inter, int64_t ld_gu,
                                           uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
@@ -24,10 +26,12 @@ hipError_t launch_gather_rows_fp8(const uint8_t* q_src, int64_t ldq_src, const f
                                   uint8_t* q_dst, int64_t ldq_dst, float* s_dst, int64_t ld_s_dst,
                                   hipStream_t stream);
 
+// pow2_scales: every scale is a power of two 2^-127 .. 2^127 (only the fp32
+// exponent fields are read; the MX-scaled MFMA applies them)
 hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
                                   const uint8_t* qw, int64_t ldw, const float* sw,
                                   uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,
-                                  hipStream_t stream);
+                                  hipStream_t stream, bool pow2_scales);
 
 // Split-K factor the dense GEMM uses for this shape (1: no split); the
 // workspace it needs is splits * m * n fp32 values.
@@ -42,6 +46,6 @@ hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, in
                                           const uint8_t* qw, const float* sw,
                                           const int32_t* group_offsets, int64_t num_groups,
                                           int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
-                                          hipStream_t stream);
+                                          hipStream_t stream, bool pow2_scales);
 
 }  // namespace fp8rl

@@ -30,19 +30,27 @@ using qmath::BlockScale;
 // Markstein step turns -0 into +0); OR-ing the sign bit of every input into its
 // code restores 0x80 there and changes nothing elsewhere.  The exhaustive
 // (x, amax) sweep of the tests checks this path against the oracle bit for bit.
-template <bool kPre>
+// How an element's quotient x / scale is formed.
+enum QuotientMode : int {
+  kMarkstein = 0,      // correctly rounded division (quant_math.hpp)
+  kMarksteinPre = 1,   // the same, block pre-scaled by 2^64 (amax < 2^-82)
+  kPow2 = 2,           // power-of-two scale: the exact product x * 2^-k
+};
+
+template <int kMode>
 __device__ __forceinline__ float quotient_of(uint32_t f32_bits, const BlockScale& bs) {
   float x = __uint_as_float(f32_bits);
-  if (kPre) x *= qmath::kPrescale;
+  if (kMode == kPow2) return x * bs.r;
+  if (kMode == kMarksteinPre) x *= qmath::kPrescale;
   return qmath::quotient(x, bs.s, bs.r);
 }
 
-template <bool kPre>
+template <int kMode>
 __device__ __forceinline__ uint32_t quant4(uint32_t w0, uint32_t w1, const BlockScale& bs) {
-  const float q0 = quotient_of<kPre>(w0 << 16, bs);
-  const float q1 = quotient_of<kPre>(w0 & 0xFFFF0000u, bs);
-  const float q2 = quotient_of<kPre>(w1 << 16, bs);
-  const float q3 = quotient_of<kPre>(w1 & 0xFFFF0000u, bs);
+  const float q0 = quotient_of<kMode>(w0 << 16, bs);
+  const float q1 = quotient_of<kMode>(w0 & 0xFFFF0000u, bs);
+  const float q2 = quotient_of<kMode>(w1 << 16, bs);
+  const float q3 = quotient_of<kMode>(w1 & 0xFFFF0000u, bs);
   int c = __builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false);   // bytes 0, 1
   c = __builtin_amdgcn_cvt_pk_fp8_f32(q2, q3, c, true);        // bytes 2, 3
   // sign bits of the four bf16 inputs (bit 15 of each half word) -> bit 7 of each byte
@@ -50,9 +58,22 @@ __device__ __forceinline__ uint32_t quant4(uint32_t w0, uint32_t w1, const Block
   return (uint32_t)c | signs;
 }
 
-template <bool kPre>
+template <int kMode>
 __device__ __forceinline__ uint2 quant8(const uint4& v, const BlockScale& bs) {
-  return make_uint2(quant4<kPre>(v.x, v.y, bs), quant4<kPre>(v.z, v.w, bs));
+  return make_uint2(quant4<kMode>(v.x, v.y, bs), quant4<kMode>(v.z, v.w, bs));
+}
+
+// 8 elements with the block's scale: the fp32 scale's two quotient paths, or the
+// power-of-two product.
+template <bool kPow2Scale>
+__device__ __forceinline__ uint2 quant8_block(const uint4& v, const BlockScale& bs) {
+  if (kPow2Scale) return quant8<kPow2>(v, bs);
+  return bs.prescaled ? quant8<kMarksteinPre>(v, bs) : quant8<kMarkstein>(v, bs);
+}
+
+template <bool kPow2Scale>
+__device__ __forceinline__ BlockScale scale_of(uint32_t amax16) {
+  return kPow2Scale ? qmath::block_scale_pow2(amax16) : qmath::block_scale(amax16);
 }
 
 // Streaming (non-temporal) 16-byte load / 8-byte store: the weight re-quantisation
@@ -76,6 +97,7 @@ __device__ __forceinline__ void store_stream8(uint8_t* p, const uint2& v) {
 // column chunk (t & 15) of rows (t >> 4) + 16 i, i = 0..7: every load instruction
 // of a wave reads four 256-byte row segments.
 // ---------------------------------------------------------------------------
+template <bool kPow2Scale>
 __global__ __launch_bounds__(256) void quant_weight_block128_kernel(
     const uint16_t* __restrict__ w, int64_t ldw, uint8_t* __restrict__ q, int64_t ldq,
     float* __restrict__ scale, int nbk) {
@@ -100,16 +122,19 @@ __global__ __launch_bounds__(256) void quant_weight_block128_kernel(
   __syncthreads();
   m = max(max(red[0], red[1]), max(red[2], red[3]));
 
-  const BlockScale bs = qmath::block_scale(m);
+  const BlockScale bs = scale_of<kPow2Scale>(m);
   if (t == 0) scale[blk] = bs.scale;
 
   uint8_t* dst = q + (int64_t)(bi * 128 + r0) * ldq + bj * 128 + chunk * 8;
-  if (bs.prescaled) {
+  if (kPow2Scale) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) store_stream8(dst + (int64_t)(16 * i) * ldq, quant8<true>(v[i], bs));
+    for (int i = 0; i < 8; ++i) store_stream8(dst + (int64_t)(16 * i) * ldq, quant8<kPow2>(v[i], bs));
+  } else if (bs.prescaled) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) store_stream8(dst + (int64_t)(16 * i) * ldq, quant8<kMarksteinPre>(v[i], bs));
   } else {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) store_stream8(dst + (int64_t)(16 * i) * ldq, quant8<false>(v[i], bs));
+    for (int i = 0; i < 8; ++i) store_stream8(dst + (int64_t)(16 * i) * ldq, quant8<kMarkstein>(v[i], bs));
   }
 }
 
@@ -118,6 +143,7 @@ __global__ __launch_bounds__(256) void quant_weight_block128_kernel(
 // consecutive (token, group) units in row-major order, so a wave reads 1 KiB of
 // contiguous row data when the four units share a token.
 // ---------------------------------------------------------------------------
+template <bool kPow2Scale>
 __global__ __launch_bounds__(256) void quant_act_token_group128_kernel(
     const uint16_t* __restrict__ a, int64_t lda, uint8_t* __restrict__ q, int64_t ldq,
     float* __restrict__ scale, int64_t ld_scale, int64_t units, int ng) {
@@ -131,8 +157,8 @@ __global__ __launch_bounds__(256) void quant_act_token_group128_kernel(
 
   const uint4 v = *reinterpret_cast<const uint4*>(a + row * lda + g * 128 + chunk * 8);
   const uint32_t m = row16_max(amax16_of(v));
-  const BlockScale bs = qmath::block_scale(m);
-  uint2 c = bs.prescaled ? quant8<true>(v, bs) : quant8<false>(v, bs);
+  const BlockScale bs = scale_of<kPow2Scale>(m);
+  const uint2 c = quant8_block<kPow2Scale>(v, bs);
   if (valid) {
     *reinterpret_cast<uint2*>(q + row * ldq + g * 128 + chunk * 8) = c;
     if (chunk == 0) scale[(int64_t)g * ld_scale + row] = bs.scale;
@@ -184,7 +210,7 @@ __global__ __launch_bounds__(256) void silu_mul_quant_group128_kernel(
     const uint4 v = silu::silu_mul8(vg[k], vu[k]);
     const uint32_t m = row16_max(amax16_of(v));
     const BlockScale bs = qmath::block_scale(m);
-    uint2 c = bs.prescaled ? quant8<true>(v, bs) : quant8<false>(v, bs);
+    const uint2 c = quant8_block<false>(v, bs);
     if (valid[k]) {
       *reinterpret_cast<uint2*>(q + row[k] * ldq + grp[k] * 128 + chunk * 8) = c;
       if (chunk == 0) scale[(int64_t)grp[k] * ld_scale + row[k]] = bs.scale;
@@ -240,22 +266,31 @@ hipError_t launch_gather_rows_fp8(const uint8_t* q_src, int64_t ldq_src, const f
 }
 
 hipError_t launch_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
-                                        uint8_t* q, int64_t ldq, float* scale, hipStream_t stream) {
+                                        uint8_t* q, int64_t ldq, float* scale, hipStream_t stream,
+                                        bool pow2_scale) {
   const int nbn = (int)(n / 128), nbk = (int)(k / 128);
   const int64_t blocks = (int64_t)nbn * nbk;
-  hipLaunchKernelGGL(quant_weight_block128_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                     w, ldw, q, ldq, scale, nbk);
+  if (pow2_scale)
+    hipLaunchKernelGGL(quant_weight_block128_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       w, ldw, q, ldq, scale, nbk);
+  else
+    hipLaunchKernelGGL(quant_weight_block128_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       w, ldw, q, ldq, scale, nbk);
   return hipGetLastError();
 }
 
 hipError_t launch_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
                                            uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
-                                           hipStream_t stream) {
+                                           hipStream_t stream, bool pow2_scale) {
   const int ng = (int)(k / 128);
   const int64_t units = m * ng;
   const int64_t blocks = (units + 15) / 16;
-  hipLaunchKernelGGL(quant_act_token_group128_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                     a, lda, q, ldq, scale, ld_scale, units, ng);
+  if (pow2_scale)
+    hipLaunchKernelGGL(quant_act_token_group128_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       a, lda, q, ldq, scale, ld_scale, units, ng);
+  else
+    hipLaunchKernelGGL(quant_act_token_group128_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       a, lda, q, ldq, scale, ld_scale, units, ng);
   return hipGetLastError();
 }
 

@@ -88,6 +88,31 @@ FP8RL_HD BlockScale block_scale(uint32_t amax16) {
   return b;
 }
 
+// Power-of-two (UE8M0) variant (section 2.4.3): scale = 2^k with k the smallest
+// integer such that amax <= 448 * 2^k, clamped below at -127 (the smallest UE8M0
+// value); 1.0 for an all-zero block.  With amax = 1.m * 2^e (a normal bf16),
+// amax / 448 = (1.m / 1.75) * 2^(e - 8), so k = e - 8, plus one when the 7-bit
+// mantissa m exceeds 0x60 (1.m > 1.75).  Subnormal amax gives k < -127 before
+// the clamp.  The element map is then the exact product x * 2^-k: s and r below
+// are 2^k and 2^-k, prescaled is false.
+FP8RL_HD int pow2_exponent(uint32_t amax16) {
+  if (amax16 == 0u) return 0;
+  const int ef = (int)(amax16 >> 7);
+  if (ef == 0) return -127;
+  const int k = ef - 127 - 8 + ((amax16 & 0x7Fu) > 0x60u ? 1 : 0);
+  return k < -127 ? -127 : k;
+}
+
+FP8RL_HD BlockScale block_scale_pow2(uint32_t amax16) {
+  const int k = pow2_exponent(amax16);                  // -127 .. 120
+  BlockScale b;
+  b.scale = as_float(k >= -126 ? (uint32_t)(k + 127) << 23 : 0x00400000u);   // 2^k (2^-127 is subnormal)
+  b.s = b.scale;
+  b.r = as_float((uint32_t)(127 - k) << 23);            // 2^-k, a normal number for every k here
+  b.prescaled = false;
+  return b;
+}
+
 // Correctly rounded fl32(a / s) for finite a (either sign), given r = fl32(1/s);
 // an exact -0 result may come back as +0 (the kernels restore the sign).
 FP8RL_HD float quotient(float a, float s, float r) {

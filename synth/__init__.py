@@ -262,12 +262,16 @@ def sweep_silu_pairs(device="cpu", exponent: int | None = 127, seed: int = 8, in
 # --------------------------------------------------------------------------
 # exhaustive element-map sweep layouts (bit patterns only)
 # --------------------------------------------------------------------------
-def _sweep_rows(per: int, device) -> torch.Tensor:
+def _sweep_rows(per: int, device, amax=None) -> torch.Tensor:
     """Rows of `per + 1` bf16 bit patterns: column 0 holds a magnitude a (the row
     maximum), the other columns list every x with |x| <= a, both signs, over as
     many rows as a needs (unused slots are +0).  Every positive finite nonzero a
-    appears, plus one all-zero row mixing +0 and -0."""
-    a = torch.arange(1, 0x7F80, dtype=torch.int32, device=device)        # positive finite magnitudes
+    appears (or every one of the given patterns), plus one all-zero row mixing +0
+    and -0."""
+    if amax is None:
+        a = torch.arange(1, 0x7F80, dtype=torch.int32, device=device)    # positive finite magnitudes
+    else:
+        a = torch.as_tensor(amax, dtype=torch.int32).to(device)
     cnt = 2 * (a + 1)                                                    # signed x with |x| <= a
     nb = (cnt + per - 1) // per
     row_a = torch.repeat_interleave(a, nb)
@@ -294,5 +298,29 @@ def sweep_weight_blocks(device="cpu") -> torch.Tensor:
 def sweep_act_groups(device="cpu") -> torch.Tensor:
     """bf16 activations [R][128]: each row one amax value plus 127 x values."""
     rows = _sweep_rows(127, device)
+    bits = torch.where(rows >= 0x8000, rows - 0x10000, rows).to(torch.int16)
+    return bits.view(torch.bfloat16)
+
+
+def sweep_group_maxima(device="cpu") -> torch.Tensor:
+    """bf16 [32640][128]: row r holds the magnitude pattern r (every finite bf16
+    magnitude, 0 included) and its negation, zeros elsewhere."""
+    a = torch.arange(0, 0x7F80, dtype=torch.int32, device=device)
+    rows = torch.zeros((a.numel(), 128), dtype=torch.int32, device=device)
+    rows[:, 0] = a
+    rows[:, 1] = a | 0x8000
+    bits = torch.where(rows >= 0x8000, rows - 0x10000, rows).to(torch.int16)
+    return bits.view(torch.bfloat16)
+
+
+def sweep_binade_groups(device="cpu", mantissas=(0x60,)) -> torch.Tensor:
+    """bf16 activations [R][128]: for every exponent field 0..254 and each given
+    7-bit mantissa, the magnitude with those bits as the row maximum, followed by
+    every x with |x| <= it (127 per row), plus the largest finite bf16 likewise."""
+    e = torch.arange(0, 255, dtype=torch.int32)
+    m = torch.as_tensor(list(mantissas), dtype=torch.int32)
+    amax = ((e[:, None] << 7) | m[None, :]).reshape(-1)
+    amax = torch.cat([amax[amax > 0], torch.tensor([0x7F7F], dtype=torch.int32)])
+    rows = _sweep_rows(127, device, amax=amax)
     bits = torch.where(rows >= 0x8000, rows - 0x10000, rows).to(torch.int16)
     return bits.view(torch.bfloat16)

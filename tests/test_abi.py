@@ -173,6 +173,29 @@ def test_gather_rows_argument_errors(lib):
     assert f(None, 128, None, 0, 0, None, 0, 128, None, 128, None, 0, None) == OK
 
 
+def test_ue8m0_entry_points_validate_like_the_fp32_ones(lib):
+    """The power-of-two variants share the argument checks of their fp32 counterparts."""
+    wq = lib.fp8rl_quant_weight_block128_ue8m0
+    assert wq(A16, 128, 200, 200, A16, 208, A16, None) == SHAPE
+    assert wq(A4, 128, 128, 128, A16, 128, A16, None) == MISALIGNED
+    assert wq(None, 128, 128, 128, A16, 128, A16, None) == INVALID
+    assert wq(None, 0, 0, 0, None, 0, None, None) == OK
+    aq = lib.fp8rl_quant_act_token_group128_ue8m0
+    assert aq(A16, 4, 128, 128, A16, 128, A16, 3, None) == INVALID
+    assert aq(A16, 4, 100, 128, A16, 128, A16, 4, None) == SHAPE
+    assert aq(A16, 4, 128, 128, A16 + 8, 128, A16, 4, None) == MISALIGNED
+    g = lib.fp8rl_gemm_w8a8_block_ue8m0
+    assert g(A16, 128, A16, 8, A16, 128, A16, A16, 128, 8, 192, 128, None) == SHAPE
+    assert g(A16, 128, A16, 7, A16, 128, A16, A16, 128, 8, 128, 128, None) == INVALID
+    assert g(A16 + 8, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == MISALIGNED
+    assert g(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None) == OK
+    gg = lib.fp8rl_grouped_gemm_w8a8_block_ue8m0
+    assert gg(A16, A16, 8, A16, A16, A16, 0, 8, A16, 128, 128, None) == INVALID
+    assert gg(A16, A16, 8, A16, A16, A16, 1025, 8, A16, 128, 128, None) == SHAPE
+    assert gg(A16, A16, 8, A4, A16, A16, 2, 8, A16, 128, 128, None) == MISALIGNED
+    assert gg(None, None, 0, None, None, None, 2, 0, None, 128, 128, None) == OK
+
+
 def test_binding_rejects_cpu_tensors():
     import torch
     import paper_2601_18150_amd as fp8rl

@@ -76,3 +76,30 @@ def test_c_element_map_equals_numpy_exhaustive():
         s = quant._scale_from_amax(quant.bf16_bits_to_f32(np.array([am], np.uint16)))[0]
         want = quant.quantize_with_scale(quant.bf16_bits_to_f32(xs), s)
         assert np.array_equal(got, want), hex(am)
+
+
+def test_c_ue8m0_quant_equals_numpy_oracle():
+    """The C power-of-two variant equals oracle/ue8m0.py on special blocks and on a
+    group for every finite bf16 magnitude (every scale exponent and the clamp)."""
+    from oracle import ue8m0
+    rng = np.random.default_rng(24)
+    x = (rng.standard_normal((256, 384)) * 0.02).astype(np.float32)
+    x[0:128, 0:128] = 0.0
+    x[0:128, 0:128][::7, ::3] = -0.0
+    x[128:256, 128:256] *= 1e36
+    x[130, 131] = -3.3895313892515355e38
+    x[0:128, 256:384] *= 1e-37
+    w = f32_to_bf16_bits(x)
+    qn, sn = ue8m0.quant_weight_block128_ue8m0(w)
+    qc, sc = cref.quant_weight_block128_ue8m0(w)
+    assert np.array_equal(qn, qc)
+    assert np.array_equal(sn.view(np.uint32), sc.view(np.uint32))
+    mags = all_finite_bf16_magnitudes()
+    a = np.zeros((mags.size, 128), np.uint16)
+    a[:, 0] = mags
+    a[:, 1] = mags | 0x8000
+    a[:, 2:] = rng.integers(0, 0x7F80, (mags.size, 126)).astype(np.uint16) % (mags[:, None].astype(np.int64) + 1)
+    qn, sn = ue8m0.quant_act_token_group128_ue8m0(a, ld_scale=mags.size + 3)
+    qc, sc = cref.quant_act_token_group128_ue8m0(a, ld_scale=mags.size + 3)
+    assert np.array_equal(qn, qc)
+    assert np.array_equal(sn.view(np.uint32), sc.view(np.uint32))
