@@ -19,7 +19,7 @@ FP8 MFMA loop with its clock.
 `cpu_baseline` times the CPU oracle on a bounded row sample of the same step.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload prefill|requant|moe|decode|mlp|moe_block|ue8m0|copy]
+                       [--workload prefill|requant|moe|decode|mlp|moe_block|ue8m0|tis|copy]
                        [--no-cpu-baseline] [--no-extra]
 """
 import argparse
@@ -46,7 +46,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe", "copy", "mlp",
-                                                              "moe_block", "ue8m0"])
+                                                              "moe_block", "ue8m0", "tis"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -418,6 +418,31 @@ def moe_block(args, fp8rl, steps=10, warmup=3):
     return res
 
 
+def tis_step(args, fp8rl, steps=20, warmup=5):
+    """Token-level TIS weights and mismatch-KL sums over one rollout batch (32 prompts x
+    16 samples x 20480 tokens, padding masked), C = 2."""
+    lt, lr, mask = synth.rollout_logprobs(device="cuda")
+    n = lt.numel()
+    w = torch.empty(n, dtype=torch.float32, device="cuda")
+    stats = torch.empty(4, dtype=torch.float64, device="cuda")
+    work = torch.empty(fp8rl.fp8rl_tis_workspace_size(n), dtype=torch.uint8, device="cuda")
+    timer = KernelTimer()
+
+    def step():
+        with timer.span("tis"):
+            fp8rl.fp8rl_tis_weights_kl(lt, lr, mask, 2.0, w_tis=w, stats=stats, workspace=work)
+
+    timed_loop(step, steps, warmup, timer)
+    ms = timer.averages_ms()["tis"]
+    nbytes = n * (4 + 4 + 1 + 4)
+    res = {"workload": f"TIS weights + mismatch-KL sums, {n} rollout tokens (32 x 16 x 20480)",
+           "avg_ms": round(ms, 5), "bytes": nbytes, "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+           "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del lt, lr, mask, w, work
+    torch.cuda.empty_cache()
+    return res
+
+
 # ---------------------------------------------------------------------------
 # decode linears of one Qwen3-8B layer (M=256): GEMM timing per linear
 # ---------------------------------------------------------------------------
@@ -602,7 +627,7 @@ def main():
                               "GB/s": hbm_copy_reference()}), flush=True)
             return
         fn = {"requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block,
-              "ue8m0": prefill_ue8m0}[args.workload]
+              "ue8m0": prefill_ue8m0, "tis": tis_step}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
     out, (a, w) = prefill(args, fp8rl)
@@ -612,7 +637,8 @@ def main():
         extra = {"weight_resync": requant(args, fp8rl), "moe_grouped": moe(args, fp8rl),
                  "decode_36_layers": decode(args, fp8rl), "prefill_ue8m0": prefill_ue8m0(args, fp8rl),
                  "dense_mlp": mlp(args, fp8rl),
-                 "moe_block": moe_block(args, fp8rl), "hbm_copy_GB/s": hbm_copy_reference(),
+                 "moe_block": moe_block(args, fp8rl), "tis": tis_step(args, fp8rl),
+                 "hbm_copy_GB/s": hbm_copy_reference(),
                  "mfma_probe": mfma_probe()}
         out["extra"] = extra
         out["roofline"]["frac_of_measured_mfma_loop"] = round(

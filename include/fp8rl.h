@@ -248,6 +248,37 @@ int fp8rl_gather_rows_fp8(const uint8_t* q_src, int64_t ldq_src, const float* s_
                           int64_t src_rows, const int32_t* index, int64_t rows, int64_t k,
                           uint8_t* q_dst, int64_t ldq_dst, float* s_dst, int64_t ld_s_dst, void* stream);
 
+/*
+ * Token-level truncated importance sampling and the mismatch KL (section 2.1.3,
+ * Eq. (2)-(3): w = pi_theta / pi_theta^FP8 per sampled token, truncated at C;
+ * section 2.2: D_KL(pi^FP8 || pi_theta) over the rollout tokens).  For each token i:
+ *
+ *   d = logp_train[i] - logp_rollout[i]  (fp64, exact),   w = e^d
+ *   w_tis[i] = fp32(min(w, clip_c)) for tokens in the mask, 0 for the others
+ *
+ * and over the tokens in the mask (fp64, deterministic order):
+ *   stats[0] = sum of -d            (KL estimate: stats[0] / stats[2])
+ *   stats[1] = sum of expm1(d) - d  (non-negative KL estimate: stats[1] / stats[2])
+ *   stats[2] = number of tokens in the mask
+ *   stats[3] = number of tokens with w > clip_c
+ *
+ * logp_train    DEVICE fp32 [n]: log-probabilities of the sampled tokens under the
+ *               bf16 training policy; logp_rollout likewise under the FP8 rollout policy
+ * mask          DEVICE uint8 [n], nonzero = token counts; NULL = every token counts
+ * clip_c        C > 0, finite (the paper uses 2)
+ * w_tis         DEVICE fp32 [n] out;  stats: DEVICE double [4] out (written also for n == 0)
+ * workspace     caller-lent device memory of at least fp8rl_tis_workspace_size(n)
+ *               bytes, 8-byte aligned, no initial contents, not shared by calls that
+ *               may overlap (else FP8RL_ERR_INVALID_ARG when missing or short)
+ * Inputs are finite (precondition).  Alignment: the fp32 arrays 16-byte, mask
+ * 4-byte, stats and workspace 8-byte aligned.
+ */
+int64_t fp8rl_tis_workspace_size(int64_t n);
+
+int fp8rl_tis_weights_kl(const float* logp_train, const float* logp_rollout, const uint8_t* mask, int64_t n,
+                         float clip_c, float* w_tis, double* stats, void* workspace, int64_t workspace_bytes,
+                         void* stream);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* fp8rl_status_string(int status);
 

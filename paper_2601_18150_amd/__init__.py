@@ -27,6 +27,7 @@ __all__ = [
     "fp8rl_quant_weight_block128_ue8m0", "fp8rl_quant_act_token_group128_ue8m0",
     "fp8rl_gemm_w8a8_block_ue8m0", "fp8rl_grouped_gemm_w8a8_block_ue8m0",
     "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8",
+    "fp8rl_tis_workspace_size", "fp8rl_tis_weights_kl",
     "fp8rl_status_string", "fp8rl_version",
     "quant_weight_block128", "quant_act_token_group128", "gemm_w8a8_block",
     "grouped_gemm_w8a8_block", "silu_mul_quant_group128", "gather_rows_fp8", "linear_w8a8",
@@ -70,12 +71,15 @@ def _load():
         "fp8rl_gemm_w8a8_block_ue8m0": [P, I, P, I, P, I, P, P, I, I, I, I, P],
         "fp8rl_grouped_gemm_w8a8_block_ue8m0": [P, P, I, P, P, P, I, I, P, I, I, P],
         "fp8rl_silu_mul_quant_group128": [P, I, I, I, P, I, P, I, P, I, P],
+        "fp8rl_tis_weights_kl": [P, P, P, I, ctypes.c_float, P, P, P, I, P],
         "fp8rl_gather_rows_fp8": [P, I, P, I, I, P, I, I, P, I, P, I, P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.fp8rl_tis_workspace_size.argtypes = [I]
+    lib.fp8rl_tis_workspace_size.restype = ctypes.c_int64
     lib.fp8rl_gemm_w8a8_block_workspace_size.argtypes = [I, I, I]
     lib.fp8rl_gemm_w8a8_block_workspace_size.restype = ctypes.c_int64
     lib.fp8rl_status_string.argtypes = [ctypes.c_int]
@@ -392,6 +396,43 @@ def fp8rl_gather_rows_fp8(q_src: torch.Tensor, s_src: torch.Tensor, index: torch
                                    ld_s_dst, _stream(stream))
     _check("fp8rl_gather_rows_fp8", st)
     return q_dst, s_dst
+
+
+def fp8rl_tis_workspace_size(n: int) -> int:
+    return int(load().fp8rl_tis_workspace_size(int(n)))
+
+
+def fp8rl_tis_weights_kl(logp_train: torch.Tensor, logp_rollout: torch.Tensor, mask: torch.Tensor | None = None,
+                         clip_c: float = 2.0, w_tis: torch.Tensor | None = None, stats: torch.Tensor | None = None,
+                         workspace: torch.Tensor | None = None, stream=None):
+    """Token-level TIS weights min(e^d, C) (0 outside the mask) and the fp64 mismatch-KL sums
+    (sum -d, sum expm1(d) - d, valid tokens, truncated tokens) of d = logp_train - logp_rollout.
+    Returns (w_tis fp32 [n], stats fp64 [4]); the workspace is allocated when not supplied."""
+    if logp_train.dtype != torch.float32 or logp_rollout.dtype != torch.float32:
+        raise TypeError("log-probabilities must be fp32")
+    if logp_train.dim() != 1 or logp_train.shape != logp_rollout.shape:
+        raise ValueError("logp_train and logp_rollout must be 1-D of one length")
+    if not logp_train.is_contiguous() or not logp_rollout.is_contiguous():
+        raise ValueError("log-probabilities must be contiguous")
+    n = logp_train.numel()
+    dev = logp_train.device
+    if mask is not None and (mask.dtype not in (torch.uint8, torch.bool) or mask.shape != logp_train.shape
+                             or not mask.is_contiguous()):
+        raise ValueError("mask must be a contiguous uint8/bool tensor of the same length")
+    if w_tis is None:
+        w_tis = torch.empty(n, dtype=torch.float32, device=dev)
+    if stats is None:
+        stats = torch.empty(4, dtype=torch.float64, device=dev)
+    need = fp8rl_tis_workspace_size(n)
+    if workspace is None:
+        workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=dev)
+    _dev(logp_train, logp_rollout, w_tis, stats, workspace, *([mask] if mask is not None else []))
+    mp = None if mask is None else mask.view(torch.uint8).data_ptr()
+    st = load().fp8rl_tis_weights_kl(logp_train.data_ptr(), logp_rollout.data_ptr(), mp, n, float(clip_c),
+                                     w_tis.data_ptr(), stats.data_ptr(), workspace.data_ptr(),
+                                     workspace.numel() * workspace.element_size(), _stream(stream))
+    _check("fp8rl_tis_weights_kl", st)
+    return w_tis, stats
 
 
 # short aliases

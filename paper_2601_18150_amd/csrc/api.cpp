@@ -211,4 +211,24 @@ static int grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint
                                                           total_rows, y, n, k, as_stream(stream), pow2));
 }
 
+int64_t fp8rl_tis_workspace_size(int64_t n) {
+  if (n < 0) return 0;
+  return int64_t(fp8rl::tis_blocks(n)) * 4 * int64_t(sizeof(double));
+}
+
+int fp8rl_tis_weights_kl(const float* logp_train, const float* logp_rollout, const uint8_t* mask, int64_t n,
+                         float clip_c, float* w_tis, double* stats, void* workspace, int64_t workspace_bytes,
+                         void* stream) {
+  if (n < 0 || !(clip_c > 0.0f) || !(clip_c <= 3.4028234663852886e38f)) return FP8RL_ERR_INVALID_ARG;
+  if (n >= (int64_t(1) << 48)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (!stats || !workspace) return FP8RL_ERR_INVALID_ARG;
+  if (n > 0 && (!logp_train || !logp_rollout || !w_tis)) return FP8RL_ERR_INVALID_ARG;
+  if (workspace_bytes < fp8rl_tis_workspace_size(n)) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(logp_train, 16) || !aligned(logp_rollout, 16) || !aligned(w_tis, 16) || !aligned(mask, 4) ||
+      !aligned(stats, 8) || !aligned(workspace, 8))
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_tis_weights_kl(logp_train, logp_rollout, mask, n, clip_c, w_tis, stats,
+                                                 static_cast<double*>(workspace), as_stream(stream)));
+}
+
 }  // extern "C"

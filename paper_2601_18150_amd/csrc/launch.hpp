@@ -48,4 +48,11 @@ hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, in
                                           int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
                                           hipStream_t stream, bool pow2_scales);
 
+// Token-level TIS weights and mismatch-KL sums: workgroups of the first pass
+// (each leaves 4 doubles of partial sums in `partial`), then one that adds them.
+int tis_blocks(int64_t n);
+
+hipError_t launch_tis_weights_kl(const float* logp_train, const float* logp_rollout, const uint8_t* mask, int64_t n,
+                                 float clip_c, float* w_tis, double* stats, double* partial, hipStream_t stream);
+
 }  // namespace fp8rl

@@ -324,3 +324,27 @@ def sweep_binade_groups(device="cpu", mantissas=(0x60,)) -> torch.Tensor:
     rows = _sweep_rows(127, device, amax=amax)
     bits = torch.where(rows >= 0x8000, rows - 0x10000, rows).to(torch.int16)
     return bits.view(torch.bfloat16)
+
+
+# --------------------------------------------------------------------------
+# rollout token log-probabilities (TIS weights / mismatch KL)
+# --------------------------------------------------------------------------
+def rollout_logprobs(seed: int = 9, device="cpu", prompts: int = 32, samples: int = 16, max_len: int = 20480,
+                     mismatch_std: float = 0.05):
+    """Per-token log-probabilities of a rollout batch laid out [prompts*samples][max_len]
+    (flattened): response lengths log-uniform in [256, max_len]; the rollout policy's
+    log-probability of each sampled token is -Exp(mean 0.4) (most tokens confident,
+    a tail of unlikely ones), the training policy's differs by N(0, mismatch_std^2)
+    with 1% of tokens off by N(0, 1).  Returns (logp_train, logp_rollout, mask uint8)."""
+    g = _gen(seed, "cpu")
+    rows = prompts * samples
+    lengths = torch.exp(torch.empty(rows, dtype=torch.float64).uniform_(math.log(256), math.log(max_len), generator=g))
+    lengths = lengths.round().clamp(256, max_len).to(torch.int64)
+    mask = (torch.arange(max_len)[None, :] < lengths[:, None]).to(torch.uint8).reshape(-1)
+    n = rows * max_len
+    lr = -torch.empty(n, dtype=torch.float32).exponential_(1.0 / 0.4, generator=g)
+    d = torch.randn(n, generator=g, dtype=torch.float32) * mismatch_std
+    far = torch.rand(n, generator=g) < 0.01
+    d = torch.where(far, torch.randn(n, generator=g, dtype=torch.float32), d)
+    lt = (lr + d).clamp(max=0.0)
+    return lt.to(device), lr.to(device), mask.to(device)

@@ -34,7 +34,7 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for f in ("fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
               "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
-              "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8"):
+              "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8", "fp8rl_tis_weights_kl"):
         assert f in names
 
 
@@ -194,6 +194,31 @@ def test_ue8m0_entry_points_validate_like_the_fp32_ones(lib):
     assert gg(A16, A16, 8, A16, A16, A16, 1025, 8, A16, 128, 128, None) == SHAPE
     assert gg(A16, A16, 8, A4, A16, A16, 2, 8, A16, 128, 128, None) == MISALIGNED
     assert gg(None, None, 0, None, None, None, 2, 0, None, 128, 128, None) == OK
+
+
+def test_tis_argument_errors(lib):
+    f = lib.fp8rl_tis_weights_kl
+    size = lib.fp8rl_tis_workspace_size
+    size.restype = ctypes.c_int64
+    size.argtypes = [ctypes.c_int64]
+    f.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int64, ctypes.c_float] + [ctypes.c_void_p] * 3 + \
+        [ctypes.c_int64, ctypes.c_void_p]
+    assert size(0) == 32 and size(-1) == 0 and size(1000) == 32 and size(1 << 30) == 2048 * 32
+    ws = size(1000)
+    #        lt   lr  mask   n    C    w    stats ws   bytes
+    assert f(A16, A16, None, -1, 2.0, A16, A16, A16, ws, None) == INVALID
+    assert f(A16, A16, None, 1000, 0.0, A16, A16, A16, ws, None) == INVALID          # C must be > 0
+    assert f(A16, A16, None, 1000, float("inf"), A16, A16, A16, ws, None) == INVALID
+    assert f(A16, A16, None, 1000, float("nan"), A16, A16, A16, ws, None) == INVALID
+    assert f(None, A16, None, 1000, 2.0, A16, A16, A16, ws, None) == INVALID
+    assert f(A16, A16, None, 1000, 2.0, A16, None, A16, ws, None) == INVALID          # no stats
+    assert f(A16, A16, None, 1000, 2.0, A16, A16, None, ws, None) == INVALID          # no workspace
+    assert f(A16, A16, None, 1000, 2.0, A16, A16, A16, ws - 8, None) == INVALID       # short workspace
+    assert f(A16 + 2, A16, None, 1000, 2.0, A16, A16, A16, ws, None) == MISALIGNED
+    assert f(A16, A16 + 4, None, 1000, 2.0, A16, A16, A16, ws, None) == MISALIGNED   # 16-byte loads
+    assert f(A16, A16, A16 + 2, 1000, 2.0, A16, A16, A16, ws, None) == MISALIGNED    # mask 4-byte
+    assert f(A16, A16, None, 1000, 2.0, A16, A16 + 4, A16, ws, None) == MISALIGNED    # stats 8-byte
+    assert f(A16, A16, None, 1000, 2.0, A16, A16, A16 + 4, ws, None) == MISALIGNED
 
 
 def test_binding_rejects_cpu_tensors():
