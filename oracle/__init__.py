@@ -21,6 +21,8 @@ This package is a plain, slow, obviously-correct restatement of what the paper
   (section 2.4.3 "Scaling Factor: FP32 vs Power-of-2").
 * ``tis``   -- token-level truncated importance-sampling weights (section
   2.1.3, Eq. (2)-(3)) and the mismatch-KL sums over the sampled tokens.
+* ``kv``    -- the FP8 KV cache with per-step scale calibration and decode
+  attention over the paged cache (section 2.3).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import, call or execute anything in this package.  The HIP
@@ -28,4 +30,4 @@ product path never does; it shares no code, table or constant generator with
 this package.  Everything here is numpy on the CPU (plus one small C file,
 ``e4m3_sweep.c``, used only by the exhaustive element-map test).
 """
-from . import e4m3, quant, gemm, act, ue8m0, tis  # noqa: F401
+from . import e4m3, quant, gemm, act, ue8m0, tis, kv  # noqa: F401
