@@ -19,7 +19,7 @@ FP8 MFMA loop with its clock.
 `cpu_baseline` times the CPU oracle on a bounded row sample of the same step.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload prefill|requant|moe|decode|mlp|moe_block|ue8m0|tis|copy]
+                       [--workload prefill|requant|moe|decode|mlp|moe_block|ue8m0|tis|kv|copy]
                        [--no-cpu-baseline] [--no-extra]
 """
 import argparse
@@ -46,7 +46,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe", "copy", "mlp",
-                                                              "moe_block", "ue8m0", "tis"])
+                                                              "moe_block", "ue8m0", "tis", "kv"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -443,6 +443,71 @@ def tis_step(args, fp8rl, steps=20, warmup=5):
     return res
 
 
+def kv_decode(args, fp8rl, steps=10, warmup=3):
+    """One Qwen3-8B attention layer at decode (32 query heads, 8 kv heads of 128) over a
+    paged cache: 64 sequences of 4096 .. 20480 tokens (seeded), the FP8 cache against the
+    same kernel over a bf16 cache, plus the per-step calibration and the cache write."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(11)
+    batch, qh, kvh = 64, 32, 8
+    seq = torch.randint(4096, 20481, (batch,), generator=g, dtype=torch.int32)
+    pages = (seq + 15) // 16
+    nb = int(pages.sum())
+    perm = torch.randperm(nb, generator=g).to(torch.int32)
+    max_blocks = int(pages.max())
+    table = torch.zeros((batch, max_blocks), dtype=torch.int32)
+    off = 0
+    for b in range(batch):
+        table[b, :pages[b]] = perm[off:off + int(pages[b])]
+        off += int(pages[b])
+    table, seq_d = table.cuda(), seq.cuda()
+    max_seq = int(seq.max())
+    dev = torch.Generator(device="cuda")
+    dev.manual_seed(12)
+    # keys and values: N(0,1) bf16 (written page by page through the FP8 write kernel below)
+    kb = torch.randn((nb, kvh, 16, 128), generator=dev, device="cuda").to(torch.bfloat16)
+    vb = torch.randn((nb, kvh, 4, 128, 4), generator=dev, device="cuda").to(torch.bfloat16)   # value page layout
+    q = torch.randn((batch, qh, 128), generator=dev, device="cuda").to(torch.bfloat16)
+    ks = fp8rl.fp8rl_kv_calibrate_scale(kb)
+    vs = fp8rl.fp8rl_kv_calibrate_scale(vb)
+    kc = torch.empty((nb, kvh, 16, 128), dtype=torch.uint8, device="cuda")
+    vc = torch.empty((nb, kvh, 4, 128, 4), dtype=torch.uint8, device="cuda")
+    # every cache slot once, in slot order (slot = block * 16 + 4a + c)
+    tok_k = kb.permute(0, 2, 1, 3).reshape(nb * 16, kvh, 128).contiguous()
+    tok_v = vb.permute(0, 2, 4, 1, 3).reshape(nb * 16, kvh, 128).contiguous()
+    slots = torch.arange(nb * 16, dtype=torch.int64, device="cuda")
+    timer = KernelTimer()
+    sm = 1.0 / 128 ** 0.5
+    work = torch.empty(fp8rl.fp8rl_attention_decode_workspace_size(batch, qh, kvh, max_seq), dtype=torch.uint8,
+                       device="cuda")
+    out = torch.empty_like(q)
+
+    def step():
+        with timer.span("calibrate_k"):
+            fp8rl.fp8rl_kv_calibrate_scale(tok_k, scale=ks)
+        with timer.span("cache_write"):
+            fp8rl.fp8rl_kv_cache_write_fp8(tok_k, tok_v, slots, ks, vs, kc, vc)
+        with timer.span("attn_fp8"):
+            fp8rl.fp8rl_attention_decode_fp8kv(q, kc, vc, table, seq_d, max_seq, ks, vs, sm, out=out, workspace=work)
+        with timer.span("attn_bf16"):
+            fp8rl.fp8rl_attention_decode_bf16kv(q, kb, vb, table, seq_d, max_seq, sm, out=out, workspace=work)
+
+    timed_loop(step, steps, warmup, timer)
+    kern = timer.averages_ms()
+    tokens = int(seq.sum())
+    cache_fp8 = tokens * kvh * 128 * 2
+    res = {"workload": f"Qwen3-8B decode attention layer, {batch} sequences of 4096..20480 tokens ({tokens} cached "
+                       f"tokens), paged FP8 cache vs bf16 cache",
+           "kernels_ms": {k: round(v, 5) for k, v in kern.items()},
+           "attn_fp8": {"bytes": cache_fp8, "GB/s": round(cache_fp8 / (kern["attn_fp8"] * 1e-3) / 1e9, 1),
+                        "frac_hbm": round(cache_fp8 / (kern["attn_fp8"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+           "attn_bf16": {"bytes": 2 * cache_fp8, "GB/s": round(2 * cache_fp8 / (kern["attn_bf16"] * 1e-3) / 1e9, 1)},
+           "fp8_speedup_vs_bf16_cache": round(kern["attn_bf16"] / kern["attn_fp8"], 3)}
+    del kb, vb, kc, vc, tok_k, tok_v, work
+    torch.cuda.empty_cache()
+    return res
+
+
 # ---------------------------------------------------------------------------
 # decode linears of one Qwen3-8B layer (M=256): GEMM timing per linear
 # ---------------------------------------------------------------------------
@@ -627,7 +692,7 @@ def main():
                               "GB/s": hbm_copy_reference()}), flush=True)
             return
         fn = {"requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block,
-              "ue8m0": prefill_ue8m0, "tis": tis_step}[args.workload]
+              "ue8m0": prefill_ue8m0, "tis": tis_step, "kv": kv_decode}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
     out, (a, w) = prefill(args, fp8rl)
@@ -638,6 +703,7 @@ def main():
                  "decode_36_layers": decode(args, fp8rl), "prefill_ue8m0": prefill_ue8m0(args, fp8rl),
                  "dense_mlp": mlp(args, fp8rl),
                  "moe_block": moe_block(args, fp8rl), "tis": tis_step(args, fp8rl),
+                 "kv_decode_attention": kv_decode(args, fp8rl),
                  "hbm_copy_GB/s": hbm_copy_reference(),
                  "mfma_probe": mfma_probe()}
         out["extra"] = extra

@@ -279,6 +279,75 @@ int fp8rl_tis_weights_kl(const float* logp_train, const float* logp_rollout, con
                          float clip_c, float* w_tis, double* stats, void* workspace, int64_t workspace_bytes,
                          void* stream);
 
+/*
+ * FP8 KV cache (section 2.3): long-context rollouts are memory-bound, so keys and
+ * values are cached in E4M3 with one fp32 scale per layer and tensor, recalibrated
+ * at every RL step because the policy weights change (section 2.3.1).
+ *
+ * Calibration: scale = fl32(amax / 448) over x (bf16 [n], e.g. one layer's keys
+ * of the step's calibration pass); 1.0 when every value is zero.  Writes the
+ * DEVICE fp32 *scale (no host synchronisation).  workspace: caller-lent device
+ * memory of fp8rl_kv_calibrate_workspace_size(n) bytes, 4-byte aligned, not
+ * shared by overlapping calls.  x 16-byte aligned.  Inputs finite (precondition).
+ */
+int64_t fp8rl_kv_calibrate_workspace_size(int64_t n);
+
+int fp8rl_kv_calibrate_scale(const uint16_t* x, int64_t n, float* scale, void* workspace, int64_t workspace_bytes,
+                             void* stream);
+
+/*
+ * Cache write: new tokens' keys and values (bf16 [tokens][kv_heads][head_dim],
+ * contiguous) into the paged caches, codes [num_blocks][kv_heads][16][head_dim]
+ * (one kv head's 16-token block is contiguous):
+ *   code = E4M3(fl32(x / s)) rounded to nearest even, saturated at +-448,
+ * s = *k_scale / *v_scale (DEVICE fp32).  slot_mapping: DEVICE int64 [tokens],
+ * slot = block * 16 + offset; slots outside [0, num_blocks * 16) are skipped
+ * (negative: padding tokens).  head_dim must be 128.  Alignment: k, v 16-byte;
+ * caches and slot_mapping 8-byte.
+ */
+int fp8rl_kv_cache_write_fp8(const uint16_t* k, const uint16_t* v, int64_t tokens, int64_t kv_heads,
+                             int64_t head_dim, const int64_t* slot_mapping, int64_t num_blocks, const float* k_scale,
+                             const float* v_scale, uint8_t* k_cache, uint8_t* v_cache, void* stream);
+
+/*
+ * Decode attention over the paged FP8 cache, one new query token per sequence,
+ * grouped query heads (query head h reads kv head h / (q_heads / kv_heads)):
+ *   out[b][h] = softmax_t(sm_scale * q[b][h] . K_t) . V_t,
+ *   K_t = dec(k code) * (*k_scale), V_t = dec(v code) * (*v_scale),
+ * over the seq_lens[b] tokens of sequence b, whose 16-token blocks are
+ * block_table[b][0 ..].  The arithmetic is bf16 x bf16 -> fp32 for the scores
+ * (every E4M3 code is exact in bf16) and fp32 for the softmax and the values
+ * ("KV cache FP8 only": the cache, not the attention math, is FP8).
+ *
+ * q            DEVICE bf16 [batch][q_heads][128];  out: DEVICE bf16 [batch][q_heads][128]
+ * block_table  DEVICE int32 [batch][max_blocks]; seq_lens DEVICE int32 [batch]
+ * max_seq_len  an upper bound of every seq_lens[b] (precondition: tokens past it are
+ *              ignored), max_blocks * 16 >= max_seq_len; a block id outside
+ *              [0, num_blocks) is clamped into range (reads a wrong block, never
+ *              outside the cache); an empty sequence gives 0
+ * q_heads / kv_heads in {1, 2, 4, 8}; head_dim 128; batch, kv_heads <= 65535
+ * workspace    caller-lent device memory of
+ *              fp8rl_attention_decode_workspace_size(batch, q_heads, kv_heads, max_seq_len)
+ *              bytes, 16-byte aligned, not shared by overlapping calls
+ * Alignment: q and the caches 16-byte, the rest 4-byte.
+ * The _bf16kv variant reads bf16 caches of the same layout (no scales), for
+ * comparison with the FP8 cache.
+ */
+int64_t fp8rl_attention_decode_workspace_size(int64_t batch, int64_t q_heads, int64_t kv_heads,
+                                              int64_t max_seq_len);
+
+int fp8rl_attention_decode_fp8kv(const uint16_t* q, const uint8_t* k_cache, const uint8_t* v_cache, int64_t num_blocks,
+                                 const int32_t* block_table, int64_t max_blocks, const int32_t* seq_lens,
+                                 int64_t batch, int64_t q_heads, int64_t kv_heads, int64_t head_dim,
+                                 int64_t max_seq_len, const float* k_scale, const float* v_scale, float sm_scale,
+                                 uint16_t* out, void* workspace, int64_t workspace_bytes, void* stream);
+
+int fp8rl_attention_decode_bf16kv(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                  int64_t num_blocks, const int32_t* block_table, int64_t max_blocks,
+                                  const int32_t* seq_lens, int64_t batch, int64_t q_heads, int64_t kv_heads,
+                                  int64_t head_dim, int64_t max_seq_len, float sm_scale, uint16_t* out,
+                                  void* workspace, int64_t workspace_bytes, void* stream);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* fp8rl_status_string(int status);
 

@@ -12,9 +12,11 @@ Readings taken here (listed with their reasons in the project's design notes):
     calibration pass's largest magnitude / 448 (the weight rule), 1.0 if zero;
   * cache codes = E4M3(fl32(x / s)) rounded to nearest even and saturated at
     +-448 (values beyond the calibrated range clip);
-  * paged cache, our layout: codes [num_blocks][kv_heads][16][head_dim] per
-    tensor, token slot = block * 16 + offset, block_table [batch][max_blocks]
-    int32, seq_lens [batch] int32;
+  * paged cache, our layout: key codes [num_blocks][kv_heads][16][head_dim]
+    (token-major pages), value codes [num_blocks][kv_heads][4][head_dim][4]
+    (token 4a + c of dim d at [a][d][c]: four tokens of a dim adjacent), token
+    slot = block * 16 + offset, block_table [batch][max_blocks] int32, seq_lens
+    [batch] int32;
   * decode attention for one new query token per sequence with grouped query
     heads (query head h reads kv head h // (q_heads / kv_heads)):
     out = softmax(sm_scale * q . dequant(K)^T) . dequant(V), evaluated in fp64
@@ -46,20 +48,29 @@ def quantize_static(x_bits: np.ndarray, scale) -> np.ndarray:
 
 def write_cache(k_cache: np.ndarray, v_cache: np.ndarray, k_bits, v_bits, slots, k_scale, v_scale):
     """Quantise new tokens' K and V ([T][kv_heads][head_dim] bf16 bits) into the paged
-    caches ([num_blocks][kv_heads][16][head_dim] codes) at the given token slots."""
+    caches (keys [num_blocks][kv_heads][16][head_dim], values
+    [num_blocks][kv_heads][4][head_dim][4]) at the given token slots."""
     kq = quantize_static(k_bits, k_scale)
     vq = quantize_static(v_bits, v_scale)
     for t, slot in enumerate(np.asarray(slots, dtype=np.int64)):
         b, o = divmod(int(slot), BLOCK_TOKENS)
         k_cache[b, :, o, :] = kq[t]
-        v_cache[b, :, o, :] = vq[t]
+        v_cache[b, :, o // 4, :, o % 4] = vq[t]
+
+
+def page_tokens(page: np.ndarray) -> np.ndarray:
+    """One block of either cache as [16 tokens][kv_heads][head_dim]."""
+    if page.ndim == 3:                                   # keys [kv][16][dim]
+        return page.transpose(1, 0, 2)
+    kvh, _, dim, _ = page.shape                          # values [kv][4][dim][4]
+    return page.transpose(1, 3, 0, 2).reshape(BLOCK_TOKENS, kvh, dim)
 
 
 def gather_sequence(cache: np.ndarray, block_table_row, seq_len: int) -> np.ndarray:
     """Codes of one sequence's tokens in order: [seq_len][kv_heads][head_dim]."""
-    pages = [cache[int(b)].transpose(1, 0, 2) for b in block_table_row[:(seq_len + BLOCK_TOKENS - 1) // BLOCK_TOKENS]]
+    pages = [page_tokens(cache[int(b)]) for b in block_table_row[:(seq_len + BLOCK_TOKENS - 1) // BLOCK_TOKENS]]
     if not pages:
-        return np.zeros((0,) + cache.shape[1:2] + cache.shape[3:], cache.dtype)
+        return np.zeros((0, cache.shape[1], cache.shape[-2] if cache.ndim == 5 else cache.shape[-1]), cache.dtype)
     return np.concatenate(pages, axis=0)[:seq_len]
 
 

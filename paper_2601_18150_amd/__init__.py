@@ -28,6 +28,8 @@ __all__ = [
     "fp8rl_gemm_w8a8_block_ue8m0", "fp8rl_grouped_gemm_w8a8_block_ue8m0",
     "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8",
     "fp8rl_tis_workspace_size", "fp8rl_tis_weights_kl",
+    "fp8rl_kv_calibrate_scale", "fp8rl_kv_cache_write_fp8", "fp8rl_attention_decode_workspace_size",
+    "fp8rl_attention_decode_fp8kv", "fp8rl_attention_decode_bf16kv",
     "fp8rl_status_string", "fp8rl_version",
     "quant_weight_block128", "quant_act_token_group128", "gemm_w8a8_block",
     "grouped_gemm_w8a8_block", "silu_mul_quant_group128", "gather_rows_fp8", "linear_w8a8",
@@ -72,6 +74,10 @@ def _load():
         "fp8rl_grouped_gemm_w8a8_block_ue8m0": [P, P, I, P, P, P, I, I, P, I, I, P],
         "fp8rl_silu_mul_quant_group128": [P, I, I, I, P, I, P, I, P, I, P],
         "fp8rl_tis_weights_kl": [P, P, P, I, ctypes.c_float, P, P, P, I, P],
+        "fp8rl_kv_calibrate_scale": [P, I, P, P, I, P],
+        "fp8rl_kv_cache_write_fp8": [P, P, I, I, I, P, I, P, P, P, P, P],
+        "fp8rl_attention_decode_fp8kv": [P, P, P, I, P, I, P, I, I, I, I, I, P, P, ctypes.c_float, P, P, I, P],
+        "fp8rl_attention_decode_bf16kv": [P, P, P, I, P, I, P, I, I, I, I, I, ctypes.c_float, P, P, I, P],
         "fp8rl_gather_rows_fp8": [P, I, P, I, I, P, I, I, P, I, P, I, P],
     }
     for name, args in sig.items():
@@ -80,6 +86,10 @@ def _load():
         f.restype = ctypes.c_int
     lib.fp8rl_tis_workspace_size.argtypes = [I]
     lib.fp8rl_tis_workspace_size.restype = ctypes.c_int64
+    lib.fp8rl_kv_calibrate_workspace_size.argtypes = [I]
+    lib.fp8rl_kv_calibrate_workspace_size.restype = ctypes.c_int64
+    lib.fp8rl_attention_decode_workspace_size.argtypes = [I, I, I, I]
+    lib.fp8rl_attention_decode_workspace_size.restype = ctypes.c_int64
     lib.fp8rl_gemm_w8a8_block_workspace_size.argtypes = [I, I, I]
     lib.fp8rl_gemm_w8a8_block_workspace_size.restype = ctypes.c_int64
     lib.fp8rl_status_string.argtypes = [ctypes.c_int]
@@ -433,6 +443,89 @@ def fp8rl_tis_weights_kl(logp_train: torch.Tensor, logp_rollout: torch.Tensor, m
                                      workspace.numel() * workspace.element_size(), _stream(stream))
     _check("fp8rl_tis_weights_kl", st)
     return w_tis, stats
+
+
+def fp8rl_kv_calibrate_scale(x: torch.Tensor, scale: torch.Tensor | None = None,
+                             workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Per-tensor FP8 scale of a bf16 calibration tensor: fp32 [1] = amax / 448 (1.0 if zero), on the device."""
+    if x.dtype != torch.bfloat16 or not x.is_contiguous():
+        raise TypeError("x must be a contiguous bfloat16 tensor")
+    n = x.numel()
+    if scale is None:
+        scale = torch.empty(1, dtype=torch.float32, device=x.device)
+    need = int(load().fp8rl_kv_calibrate_workspace_size(n))
+    if workspace is None:
+        workspace = torch.empty(max(need, 4), dtype=torch.uint8, device=x.device)
+    _dev(x, scale, workspace)
+    st = load().fp8rl_kv_calibrate_scale(x.data_ptr(), n, scale.data_ptr(), workspace.data_ptr(),
+                                         workspace.numel() * workspace.element_size(), _stream(stream))
+    _check("fp8rl_kv_calibrate_scale", st)
+    return scale
+
+
+def fp8rl_kv_cache_write_fp8(k: torch.Tensor, v: torch.Tensor, slot_mapping: torch.Tensor, k_scale: torch.Tensor,
+                             v_scale: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor, stream=None):
+    """Quantise new tokens' k, v (bf16 [T][kv_heads][128]) into the paged caches
+    (uint8 [num_blocks][kv_heads][16][128]) at slot_mapping (int64 [T])."""
+    if k.dtype != torch.bfloat16 or v.dtype != torch.bfloat16 or k.shape != v.shape or k.dim() != 3:
+        raise TypeError("k and v must be bfloat16 [T][kv_heads][head_dim]")
+    if not (k.is_contiguous() and v.is_contiguous() and k_cache.is_contiguous() and v_cache.is_contiguous()):
+        raise ValueError("k, v and the caches must be contiguous")
+    if slot_mapping.dtype != torch.int64 or slot_mapping.numel() != k.shape[0]:
+        raise ValueError("slot_mapping must be int64 [T]")
+    t, kvh, dim = k.shape
+    k_cache, v_cache = _u8(k_cache), _u8(v_cache)
+    _dev(k, v, slot_mapping, k_scale, v_scale, k_cache, v_cache)
+    st = load().fp8rl_kv_cache_write_fp8(k.data_ptr(), v.data_ptr(), t, kvh, dim, slot_mapping.data_ptr(),
+                                         k_cache.shape[0], k_scale.data_ptr(), v_scale.data_ptr(),
+                                         k_cache.data_ptr(), v_cache.data_ptr(), _stream(stream))
+    _check("fp8rl_kv_cache_write_fp8", st)
+
+
+def fp8rl_attention_decode_workspace_size(batch: int, q_heads: int, kv_heads: int, max_seq_len: int) -> int:
+    return int(load().fp8rl_attention_decode_workspace_size(batch, q_heads, kv_heads, max_seq_len))
+
+
+def _attention(name, q, k_cache, v_cache, block_table, seq_lens, max_seq_len, sm_scale, scales, out, workspace,
+               stream):
+    if q.dtype != torch.bfloat16 or q.dim() != 3 or not q.is_contiguous():
+        raise TypeError("q must be contiguous bfloat16 [batch][q_heads][head_dim]")
+    batch, q_heads, dim = q.shape
+    num_blocks, kv_heads = k_cache.shape[0], k_cache.shape[1]
+    if block_table.dtype != torch.int32 or block_table.dim() != 2 or not block_table.is_contiguous():
+        raise ValueError("block_table must be contiguous int32 [batch][max_blocks]")
+    if seq_lens.dtype != torch.int32 or seq_lens.numel() != batch:
+        raise ValueError("seq_lens must be int32 [batch]")
+    if out is None:
+        out = torch.empty_like(q)
+    need = fp8rl_attention_decode_workspace_size(batch, q_heads, kv_heads, max_seq_len)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _dev(q, k_cache, v_cache, block_table, seq_lens, out, workspace, *scales)
+    args = [q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), num_blocks, block_table.data_ptr(),
+            block_table.shape[1], seq_lens.data_ptr(), batch, q_heads, kv_heads, dim, int(max_seq_len)]
+    args += [s.data_ptr() for s in scales]
+    args += [float(sm_scale), out.data_ptr(), workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+             _stream(stream)]
+    _check(name, getattr(load(), name)(*args))
+    return out
+
+
+def fp8rl_attention_decode_fp8kv(q, k_cache, v_cache, block_table, seq_lens, max_seq_len, k_scale, v_scale, sm_scale,
+                                 out=None, workspace=None, stream=None):
+    """Decode attention over the paged FP8 caches (uint8 [num_blocks][kv_heads][16][128]),
+    scales fp32 [1] on the device; returns bf16 [batch][q_heads][128]."""
+    return _attention("fp8rl_attention_decode_fp8kv", q, _u8(k_cache), _u8(v_cache), block_table, seq_lens,
+                      max_seq_len, sm_scale, [k_scale, v_scale], out, workspace, stream)
+
+
+def fp8rl_attention_decode_bf16kv(q, k_cache, v_cache, block_table, seq_lens, max_seq_len, sm_scale, out=None,
+                                  workspace=None, stream=None):
+    """The same decode attention over bf16 caches (bf16 [num_blocks][kv_heads][16][128])."""
+    if k_cache.dtype != torch.bfloat16 or v_cache.dtype != torch.bfloat16:
+        raise TypeError("bf16 caches expected")
+    return _attention("fp8rl_attention_decode_bf16kv", q, k_cache, v_cache, block_table, seq_lens, max_seq_len,
+                      sm_scale, [], out, workspace, stream)
 
 
 # short aliases

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libfp8rl.so")
 PROBE_LIB = os.path.join(HERE, "libfp8rl_probe.so")
 OBJDIR = os.path.join(ROOT, "_build")
-SOURCES = ["quant.hip", "gemm.hip", "tis.hip", "api.cpp"]
+SOURCES = ["quant.hip", "gemm.hip", "tis.hip", "kv.hip", "api.cpp"]
 PROBE_SOURCES = ["probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -231,4 +231,86 @@ int fp8rl_tis_weights_kl(const float* logp_train, const float* logp_rollout, con
                                                  static_cast<double*>(workspace), as_stream(stream)));
 }
 
+int64_t fp8rl_kv_calibrate_workspace_size(int64_t n) {
+  return n < 0 ? 0 : int64_t(fp8rl::kv_amax_blocks(n)) * 4;
+}
+
+int fp8rl_kv_calibrate_scale(const uint16_t* x, int64_t n, float* scale, void* workspace, int64_t workspace_bytes,
+                             void* stream) {
+  if (n < 0 || !scale || !workspace || (n > 0 && !x)) return FP8RL_ERR_INVALID_ARG;
+  if (n >= (int64_t(1) << 46)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (workspace_bytes < fp8rl_kv_calibrate_workspace_size(n)) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(scale, 4) || !aligned(workspace, 4)) return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_kv_calibrate_scale(x, n, scale, static_cast<uint32_t*>(workspace),
+                                                     as_stream(stream)));
+}
+
+int fp8rl_kv_cache_write_fp8(const uint16_t* k, const uint16_t* v, int64_t tokens, int64_t kv_heads,
+                             int64_t head_dim, const int64_t* slot_mapping, int64_t num_blocks, const float* k_scale,
+                             const float* v_scale, uint8_t* k_cache, uint8_t* v_cache, void* stream) {
+  if (tokens < 0 || kv_heads < 1 || num_blocks < 0) return FP8RL_ERR_INVALID_ARG;
+  if (head_dim != 128 || kv_heads > 1024 || tokens >= (int64_t(1) << 31)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (tokens == 0) return FP8RL_OK;
+  if (!k || !v || !slot_mapping || !k_scale || !v_scale || !k_cache || !v_cache) return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(k, 16) || !aligned(v, 16) || !aligned(k_cache, 8) || !aligned(v_cache, 8) || !aligned(slot_mapping, 8) ||
+      !aligned(k_scale, 4) || !aligned(v_scale, 4))
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_kv_cache_write(k, v, tokens, (int)kv_heads, slot_mapping, num_blocks, k_scale,
+                                                 v_scale, k_cache, v_cache, as_stream(stream)));
+}
+
+int64_t fp8rl_attention_decode_workspace_size(int64_t batch, int64_t q_heads, int64_t kv_heads,
+                                              int64_t max_seq_len) {
+  if (batch < 0 || kv_heads < 1 || q_heads < kv_heads || q_heads % kv_heads || max_seq_len < 0) return 0;
+  const fp8rl::AttnSplit sp = fp8rl::attn_decode_split(batch, kv_heads, q_heads / kv_heads, max_seq_len);
+  return batch * kv_heads * int64_t(sp.max_splits) * sp.partial_floats * 4;
+}
+
+static int attention_decode(const uint16_t* q, const void* k_cache, const void* v_cache, bool fp8, int64_t num_blocks,
+                            const int32_t* block_table, int64_t max_blocks, const int32_t* seq_lens, int64_t batch,
+                            int64_t q_heads, int64_t kv_heads, int64_t head_dim, int64_t max_seq_len,
+                            const float* k_scale, const float* v_scale, float sm_scale, uint16_t* out,
+                            void* workspace, int64_t workspace_bytes, void* stream) {
+  if (batch < 0 || kv_heads < 1 || q_heads < 1 || max_seq_len < 0 || max_blocks < 0 || num_blocks < 0)
+    return FP8RL_ERR_INVALID_ARG;
+  if (!(sm_scale > 0.0f) || !(sm_scale <= 3.4028234663852886e38f)) return FP8RL_ERR_INVALID_ARG;
+  if (head_dim != 128 || q_heads % kv_heads) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  const int64_t group = q_heads / kv_heads;
+  if (group != 1 && group != 2 && group != 4 && group != 8) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (batch > 65535 || kv_heads > 65535 || max_seq_len >= (int64_t(1) << 30)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (batch == 0) return FP8RL_OK;
+  if (!q || !k_cache || !v_cache || !block_table || !seq_lens || !out || !workspace) return FP8RL_ERR_INVALID_ARG;
+  if (fp8 && (!k_scale || !v_scale)) return FP8RL_ERR_INVALID_ARG;
+  if (num_blocks < 1 || max_blocks < 1 || max_blocks * 16 < max_seq_len) return FP8RL_ERR_INVALID_ARG;
+  if (workspace_bytes < fp8rl_attention_decode_workspace_size(batch, q_heads, kv_heads, max_seq_len))
+    return FP8RL_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(block_table, 4) ||
+      !aligned(seq_lens, 4) || !aligned(out, 4) || !aligned(workspace, 16) || !aligned(k_scale, 4) ||
+      !aligned(v_scale, 4))
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_attention_decode(q, k_cache, v_cache, fp8, num_blocks, block_table, max_blocks,
+                                                   seq_lens, batch, q_heads, kv_heads, max_seq_len, k_scale, v_scale,
+                                                   sm_scale, out, static_cast<float*>(workspace), as_stream(stream)));
+}
+
+int fp8rl_attention_decode_fp8kv(const uint16_t* q, const uint8_t* k_cache, const uint8_t* v_cache, int64_t num_blocks,
+                                 const int32_t* block_table, int64_t max_blocks, const int32_t* seq_lens,
+                                 int64_t batch, int64_t q_heads, int64_t kv_heads, int64_t head_dim,
+                                 int64_t max_seq_len, const float* k_scale, const float* v_scale, float sm_scale,
+                                 uint16_t* out, void* workspace, int64_t workspace_bytes, void* stream) {
+  return attention_decode(q, k_cache, v_cache, true, num_blocks, block_table, max_blocks, seq_lens, batch, q_heads,
+                          kv_heads, head_dim, max_seq_len, k_scale, v_scale, sm_scale, out, workspace,
+                          workspace_bytes, stream);
+}
+
+int fp8rl_attention_decode_bf16kv(const uint16_t* q, const uint16_t* k_cache, const uint16_t* v_cache,
+                                  int64_t num_blocks, const int32_t* block_table, int64_t max_blocks,
+                                  const int32_t* seq_lens, int64_t batch, int64_t q_heads, int64_t kv_heads,
+                                  int64_t head_dim, int64_t max_seq_len, float sm_scale, uint16_t* out,
+                                  void* workspace, int64_t workspace_bytes, void* stream) {
+  return attention_decode(q, k_cache, v_cache, false, num_blocks, block_table, max_blocks, seq_lens, batch, q_heads,
+                          kv_heads, head_dim, max_seq_len, nullptr, nullptr, sm_scale, out, workspace,
+                          workspace_bytes, stream);
+}
+
 }  // extern "C"

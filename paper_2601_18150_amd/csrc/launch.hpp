@@ -55,4 +55,29 @@ int tis_blocks(int64_t n);
 hipError_t launch_tis_weights_kl(const float* logp_train, const float* logp_rollout, const uint8_t* mask, int64_t n,
                                  float clip_c, float* w_tis, double* stats, double* partial, hipStream_t stream);
 
+// FP8 KV cache: per-tensor scale calibration (workgroup maxima in `partial`,
+// kv_amax_blocks(n) words), quantised writes into the paged cache, and decode
+// attention over it (fp8_cache false: the same kernel over a bf16 cache).
+int kv_amax_blocks(int64_t n);
+
+hipError_t launch_kv_calibrate_scale(const uint16_t* x, int64_t n, float* scale, uint32_t* partial,
+                                     hipStream_t stream);
+
+hipError_t launch_kv_cache_write(const uint16_t* k, const uint16_t* v, int64_t tokens, int kv_heads,
+                                 const int64_t* slots, int64_t num_blocks, const float* k_scale, const float* v_scale,
+                                 uint8_t* k_cache, uint8_t* v_cache, hipStream_t stream);
+
+struct AttnSplit {
+  int split_tokens;      // tokens per wave (a multiple of 16)
+  int max_splits;        // splits of the longest sequence
+  int partial_floats;    // floats per (sequence, kv head, split) record
+};
+AttnSplit attn_decode_split(int64_t batch, int64_t kv_heads, int64_t group, int64_t max_seq_len);
+
+hipError_t launch_attention_decode(const uint16_t* q, const void* k_cache, const void* v_cache, bool fp8_cache,
+                                   int64_t num_blocks, const int32_t* block_table, int64_t max_blocks,
+                                   const int32_t* seq_lens, int64_t batch, int64_t q_heads, int64_t kv_heads,
+                                   int64_t max_seq_len, const float* k_scale, const float* v_scale, float sm_scale,
+                                   uint16_t* out, float* partial, hipStream_t stream);
+
 }  // namespace fp8rl

@@ -19,9 +19,9 @@ def random_paged(rng, batch, kv_heads, dim, seq_lens, spare=3):
     for b, p in enumerate(pages):
         table[b, :p] = perm[k:k + p]
         k += p
-    codes = lambda: (lambda c: np.where((c & 0x7F) == 0x7F, c ^ 1, c))(
-        rng.integers(0, 256, (num_blocks, kv_heads, 16, dim)).astype(np.uint8))
-    return codes(), codes(), table
+    codes = lambda shape: (lambda c: np.where((c & 0x7F) == 0x7F, c ^ 1, c))(
+        rng.integers(0, 256, shape).astype(np.uint8))
+    return codes((num_blocks, kv_heads, 16, dim)), codes((num_blocks, kv_heads, 4, dim, 4)), table
 
 
 def test_decode_attention_matches_torch_sdpa_with_grouped_heads():
@@ -50,7 +50,7 @@ def test_decode_attention_closed_forms():
     batch, q_heads, kv_heads, dim = 2, 4, 1, 128
     kc = np.full((4, kv_heads, 16, dim), 0x38, np.uint8)          # every key = 1.0 * scale
     rng = np.random.default_rng(2)
-    vc = rng.integers(0, 0x7E, (4, kv_heads, 16, dim)).astype(np.uint8)
+    vc = rng.integers(0, 0x7E, (4, kv_heads, 4, dim, 4)).astype(np.uint8)
     table = np.array([[0, 1, 2, 3], [3, 2, 1, 0]], np.int32)
     seq_lens = np.array([50, 64], np.int32)
     q = bf16_bits(rng.standard_normal((batch, q_heads, dim)))
@@ -63,7 +63,7 @@ def test_decode_attention_closed_forms():
     kc2[2, 0, 5, :] = 0x70                                        # token 2*16+5 of sequence 0 (one key of 256)
     q2 = bf16_bits(np.ones((1, q_heads, dim)))
     out2 = kv.attention_decode(q2, kc2, vc, 1.0, 0.5, table[:1], seq_lens[:1], 1.0)
-    v0 = e4m3.decode(vc[2, 0, 5, :]) * 0.5
+    v0 = e4m3.decode(vc[2, 0, 1, :, 1]) * 0.5                      # token 5 of the block: [5 // 4][:][5 % 4]
     assert np.allclose(out2[0, 0], v0, rtol=0, atol=1e-12)
 
 
@@ -93,11 +93,18 @@ def test_calibrated_scale_maps_the_maximum_to_448():
     assert kv.calibrate_scale(np.zeros(8, np.uint16)) == 1.0
 
 
+def test_value_page_layout_puts_four_tokens_of_a_dim_together():
+    page = np.arange(2 * 16 * 128, dtype=np.int64).reshape(2, 4, 128, 4)    # [kv][4][dim][4]
+    tok = kv.page_tokens(page)
+    assert tok.shape == (16, 2, 128)
+    assert tok[5, 1, 7] == page[1, 1, 7, 1] and tok[12, 0, 127] == page[0, 3, 127, 0]
+
+
 def test_cache_write_then_gather_round_trips_tokens_in_order():
     rng = np.random.default_rng(5)
     kv_heads, dim = 3, 128
     kc = np.zeros((6, kv_heads, 16, dim), np.uint8)
-    vc = np.zeros_like(kc)
+    vc = np.zeros((6, kv_heads, 4, dim, 4), np.uint8)
     table = np.array([4, 1, 5], np.int32)
     n = 40
     slots = np.array([table[t // 16] * 16 + t % 16 for t in range(n)])
