@@ -103,7 +103,8 @@ int fp8rl_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int6
  * n, k multiples of 128; m >= 0 arbitrary (m == 0 is a no-op); at most 2^30
  * output tiles of 128 x 128 (ceil(m/128) * n/128), else FP8RL_ERR_UNSUPPORTED_SHAPE.
  * Alignment: qa, qw, y 16-byte aligned; lda % 16 == 0; ldw % 16 == 0; ldy % 8 == 0;
- * sa, sw 4-byte aligned.  lda >= k, ldw >= k, ldy >= n, ld_sa >= m.
+ * sa, sw 4-byte aligned.  lda >= k, ldw >= k, ldy >= n, ld_sa >= m;
+ * lda, ldw < 2^24 (else FP8RL_ERR_UNSUPPORTED_SHAPE).
  */
 int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
                           const uint8_t* qw, int64_t ldw, const float* sw,
@@ -157,8 +158,8 @@ int fp8rl_gemm_w8a8_block_ws(const uint8_t* qa, int64_t lda, const float* sa, in
  *               offsets[num_groups] == total_rows (precondition, not checked:
  *               checking would need a device read)
  * y             [total_rows][n] bf16 out, contiguous
- * n, k multiples of 128; 1 <= num_groups <= 1024 (more: FP8RL_ERR_UNSUPPORTED_SHAPE);
- * total_rows >= 0 (0 is a no-op).
+ * n, k multiples of 128, k < 2^24; 1 <= num_groups <= 1024 (else
+ * FP8RL_ERR_UNSUPPORTED_SHAPE); total_rows >= 0 (0 is a no-op).
  * Alignment: qa, qw, y 16-byte aligned; k % 16 == 0 follows from k % 128 == 0.
  */
 int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,

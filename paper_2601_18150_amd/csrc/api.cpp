@@ -10,6 +10,7 @@
 namespace {
 
 constexpr int64_t kMaxDim = int64_t(1) << 31;   // per-dimension limit (32-bit tile indices)
+constexpr int64_t kMaxLd = int64_t(1) << 24;     // GEMM operand row pitch limit (32-bit in-tile DMA offsets)
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -31,6 +32,7 @@ int check_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, 
   if (!qa || !sa || !qw || !sw || !y) return FP8RL_ERR_INVALID_ARG;
   if (k == 0) return FP8RL_ERR_UNSUPPORTED_SHAPE;   // an empty reduction is not a blockwise GEMM
   if (lda < k || ldw < k || ldy < n || ld_sa < m) return FP8RL_ERR_INVALID_ARG;
+  if (lda >= kMaxLd || ldw >= kMaxLd) return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (!aligned(qa, 16) || !aligned(qw, 16) || !aligned(y, 16) || !aligned(sa, 4) || !aligned(sw, 4) ||
       lda % 16 || ldw % 16 || ldy % 8)
     return FP8RL_ERR_MISALIGNED;
@@ -197,7 +199,7 @@ static int grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint
   if (total_rows < 0 || n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
   if (num_groups < 1) return FP8RL_ERR_INVALID_ARG;
   if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
-  if (total_rows >= kMaxDim || n >= kMaxDim || k >= kMaxDim || num_groups > 1024 ||
+  if (total_rows >= kMaxDim || n >= kMaxDim || k >= kMaxLd || num_groups > 1024 ||
       (total_rows / 128 + num_groups) * (n / 128) >= (int64_t(1) << 31))
     return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (total_rows == 0 || n == 0) return FP8RL_OK;

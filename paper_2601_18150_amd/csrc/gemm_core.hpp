@@ -109,6 +109,22 @@ __device__ __forceinline__ void lds_dma4(const float* gptr, uint8_t* lds_wave_ba
   __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 4, 0, 0);
 }
 
+// Raw buffer resource at base (stride 0, range 4 GiB - 1, so no offset used
+// here is clamped: the DMA offsets are relative to a tile's first row, at most
+// 256 rows x a leading dimension below 2^24 plus K).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, 0x00020000);
+}
+
+// The 16-byte DMA through a buffer resource (buffer_load_dwordx4 ... lds): lane
+// address = base + voff + soff, with a 32-bit per-lane offset (one VGPR) and a
+// wave-uniform one (an SGPR).  Used in the K loop, where the 64-bit per-lane
+// addresses of global_load_lds would hold two VGPRs per load.
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                          uint8_t* lds_wave_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_wave_base, 16, voff, soff, 0, 0);
+}
+
 // 16-byte streaming (non-temporal) store of eight bf16
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void store_stream16(uint16_t* p, const uint4& v) {
@@ -268,16 +284,19 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       const bool last = kb + 1 == KB;
       const bool refill = !last || has_nxt;
       uint8_t* dslot = lds + (slot ^ 1) * C::kStageBytes;
-      const uint8_t* dwb = wbase + (kb + 1) * 128;
-      const uint8_t* dab = abase + (kb + 1) * 128;
+      const uint8_t* dwb = wbase;
+      const uint8_t* dab = abase;
+      uint32_t dsoff = (kb + 1) * 128;
       const float* dsa = sa_lane + (int64_t)(kb + 1) * ld_sa;
       if constexpr (kCross) {
         if (last) {
           dwb = qw + nxt.qw_off + (int64_t)nxt.n0 * ldw;
           dab = qa + (int64_t)nxt.row_lo * lda;
+          dsoff = 0;
           dsa = sa_lane_of(nxt);
         }
       }
+      const __amdgpu_buffer_rsrc_t rw = buffer_rsrc(dwb), ra = buffer_rsrc(dab);
 
       constexpr int kDmaSpread = C::TN >= 8 ? C::TN / 2 : 1;   // sub-tile rows that carry DMA issue
       const uint8_t* st = lds + slot * C::kStageBytes;
@@ -315,7 +334,7 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
             const int o = wave + i * C::kWaves;
             uint32_t off = goff[i];
             if constexpr (kCross) off = last ? goff_n[i] : goff[i];
-            lds_dma16((o < C::BN / 8 ? dwb : dab) + off, dslot + o * 1024);
+            lds_dma16(o < C::BN / 8 ? rw : ra, off, dsoff, dslot + o * 1024);
           }
         }
         if (tn == 0 && sdma && refill) lds_dma4(dsa, dslot + C::kWBytes + C::kABytes + wave * 256);

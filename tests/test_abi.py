@@ -96,6 +96,8 @@ def test_gemm_argument_errors(lib):
     assert f(A16 + 8, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == MISALIGNED
     assert f(A16, 136, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == MISALIGNED
     assert f(A16, 128, A16, 8, A16, 128, A16, A16, 132, 8, 128, 128, None) == MISALIGNED
+    assert f(A16, 1 << 24, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == SHAPE   # row pitch limit
+    assert f(A16, 128, A16, 8, A16, 1 << 24, A16, A16, 128, 8, 128, 128, None) == SHAPE
     assert f(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None) == OK
 
 
@@ -131,6 +133,7 @@ def test_grouped_gemm_argument_errors(lib):
     assert f(A16, A16, 8, A16, A16, A16, 2, -1, A16, 128, 128, None) == INVALID
     assert f(A16, A16, 8, A16, A16, A16, 2, 8, A16, 192, 128, None) == SHAPE
     assert f(A16, A16, 8, A16, A16, A16, 1025, 8, A16, 128, 128, None) == SHAPE   # over 1024 experts
+    assert f(A16, A16, 8, A16, A16, A16, 2, 8, A16, 128, 1 << 24, None) == SHAPE  # k at the row pitch limit
     assert f(A16, A16, 7, A16, A16, A16, 2, 8, A16, 128, 128, None) == INVALID    # ld_sa < R
     assert f(A16, A16, 8, A16, A16, None, 2, 8, A16, 128, 128, None) == INVALID
     assert f(A16, A16, 8, A16, A16, A16 + 2, 2, 8, A16, 128, 128, None) == MISALIGNED
