@@ -496,12 +496,19 @@ def kv_decode(args, fp8rl, steps=10, warmup=3):
     kern = timer.averages_ms()
     tokens = int(seq.sum())
     cache_fp8 = tokens * kvh * 128 * 2
+    write_bytes = nb * 16 * kvh * 128 * (2 + 2 + 1 + 1)      # bf16 K and V in, their codes out (every slot)
+    calib_bytes = nb * 16 * kvh * 128 * 2                    # bf16 keys read
     res = {"workload": f"Qwen3-8B decode attention layer, {batch} sequences of 4096..20480 tokens ({tokens} cached "
                        f"tokens), paged FP8 cache vs bf16 cache",
            "kernels_ms": {k: round(v, 5) for k, v in kern.items()},
            "attn_fp8": {"bytes": cache_fp8, "GB/s": round(cache_fp8 / (kern["attn_fp8"] * 1e-3) / 1e9, 1),
                         "frac_hbm": round(cache_fp8 / (kern["attn_fp8"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
            "attn_bf16": {"bytes": 2 * cache_fp8, "GB/s": round(2 * cache_fp8 / (kern["attn_bf16"] * 1e-3) / 1e9, 1)},
+           "cache_write": {"tokens": nb * 16, "bytes": write_bytes,
+                           "GB/s": round(write_bytes / (kern["cache_write"] * 1e-3) / 1e9, 1),
+                           "frac_hbm": round(write_bytes / (kern["cache_write"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+           "calibrate_k": {"bytes": calib_bytes, "GB/s": round(calib_bytes / (kern["calibrate_k"] * 1e-3) / 1e9, 1),
+                           "frac_hbm": round(calib_bytes / (kern["calibrate_k"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
            "fp8_speedup_vs_bf16_cache": round(kern["attn_bf16"] / kern["attn_fp8"], 3)}
     del kb, vb, kc, vc, tok_k, tok_v, work
     torch.cuda.empty_cache()

@@ -298,13 +298,19 @@ int fp8rl_kv_calibrate_scale(const uint16_t* x, int64_t n, float* scale, void* w
 
 /*
  * Cache write: new tokens' keys and values (bf16 [tokens][kv_heads][head_dim],
- * contiguous) into the paged caches, codes [num_blocks][kv_heads][16][head_dim]
- * (one kv head's 16-token block is contiguous):
+ * contiguous) into the paged caches (one kv head's 16-token block is contiguous
+ * in both):
+ *   k_cache [num_blocks][kv_heads][16][head_dim]       token o of a block at [o][d]
+ *   v_cache [num_blocks][kv_heads][4][head_dim][4]     token o at [o / 4][d][o % 4]
+ * (the value layout puts four tokens of one dim in one dword, the operand order
+ * of the attention kernel's value product), with
  *   code = E4M3(fl32(x / s)) rounded to nearest even, saturated at +-448,
  * s = *k_scale / *v_scale (DEVICE fp32).  slot_mapping: DEVICE int64 [tokens],
  * slot = block * 16 + offset; slots outside [0, num_blocks * 16) are skipped
- * (negative: padding tokens).  head_dim must be 128.  Alignment: k, v 16-byte;
- * caches and slot_mapping 8-byte.
+ * (negative: padding tokens); two tokens with one slot: which one's codes land
+ * is unspecified.  head_dim must be 128; ceil(tokens / 4) * kv_heads * 16 < 2^31
+ * (else FP8RL_ERR_UNSUPPORTED_SHAPE).  Alignment: k, v 16-byte; caches and
+ * slot_mapping 8-byte.
  */
 int fp8rl_kv_cache_write_fp8(const uint16_t* k, const uint16_t* v, int64_t tokens, int64_t kv_heads,
                              int64_t head_dim, const int64_t* slot_mapping, int64_t num_blocks, const float* k_scale,
@@ -320,6 +326,7 @@ int fp8rl_kv_cache_write_fp8(const uint16_t* k, const uint16_t* v, int64_t token
  * (every E4M3 code is exact in bf16) and fp32 for the softmax and the values
  * ("KV cache FP8 only": the cache, not the attention math, is FP8).
  *
+ * k_cache, v_cache  the layouts written by fp8rl_kv_cache_write_fp8
  * q            DEVICE bf16 [batch][q_heads][128];  out: DEVICE bf16 [batch][q_heads][128]
  * block_table  DEVICE int32 [batch][max_blocks]; seq_lens DEVICE int32 [batch]
  * max_seq_len  an upper bound of every seq_lens[b] (precondition: tokens past it are

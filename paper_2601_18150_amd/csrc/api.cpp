@@ -251,7 +251,9 @@ int fp8rl_kv_cache_write_fp8(const uint16_t* k, const uint16_t* v, int64_t token
                              int64_t head_dim, const int64_t* slot_mapping, int64_t num_blocks, const float* k_scale,
                              const float* v_scale, uint8_t* k_cache, uint8_t* v_cache, void* stream) {
   if (tokens < 0 || kv_heads < 1 || num_blocks < 0) return FP8RL_ERR_INVALID_ARG;
-  if (head_dim != 128 || kv_heads > 1024 || tokens >= (int64_t(1) << 31)) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (head_dim != 128 || kv_heads > 1024 || tokens >= (int64_t(1) << 31) ||
+      (tokens + 3) / 4 * kv_heads * 16 >= (int64_t(1) << 31))
+    return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (tokens == 0) return FP8RL_OK;
   if (!k || !v || !slot_mapping || !k_scale || !v_scale || !k_cache || !v_cache) return FP8RL_ERR_INVALID_ARG;
   if (!aligned(k, 16) || !aligned(v, 16) || !aligned(k_cache, 8) || !aligned(v_cache, 8) || !aligned(slot_mapping, 8) ||

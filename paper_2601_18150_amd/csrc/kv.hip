@@ -70,10 +70,14 @@ __global__ __launch_bounds__(64) void scale_final_kernel(const uint32_t* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Cache write: one thread per 8 values (token, kv head, 8-dim chunk) of K and V.
-// code = E4M3(fl32(x / s)) saturated at +-448 (IEEE division; the sign of x is
-// OR-ed back so that -0 gives 0x80).  Slots outside [0, num_blocks * 16) are
-// skipped (negative slots mark padding tokens).
+// Cache write: one thread per (four consecutive tokens, kv head, 8-dim chunk)
+// of K and V.  code = E4M3(fl32(x / s)) saturated at +-448 (IEEE division; the
+// sign of x is OR-ed back so that -0 gives 0x80).  Slots outside
+// [0, num_blocks * 16) are skipped (negative slots mark padding tokens).
+// When the four tokens go to four consecutive slots starting at a multiple of 4
+// (a prefill's tokens, in order), their value codes fill whole dwords of the
+// value page (dim d: tokens 4a .. 4a+3) and are stored as 32 contiguous bytes;
+// otherwise each token's value codes are stored byte by byte.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t quant4_static(uint32_t w0, uint32_t w1, float s) {
   float q[4] = {__uint_as_float(w0 << 16), __uint_as_float(w0 & 0xFFFF0000u), __uint_as_float(w1 << 16),
@@ -86,34 +90,67 @@ __device__ __forceinline__ uint32_t quant4_static(uint32_t w0, uint32_t w1, floa
   return (uint32_t)c | signs;
 }
 
+// byte j of the result = byte `b` of word j (4x4 byte transpose, one output word)
+__device__ __forceinline__ uint32_t gather_byte(const uint32_t (&w)[4], int b) {
+  return ((w[0] >> (8 * b)) & 0xFFu) | (((w[1] >> (8 * b)) & 0xFFu) << 8) | (((w[2] >> (8 * b)) & 0xFFu) << 16) |
+         (((w[3] >> (8 * b)) & 0xFFu) << 24);
+}
+
 __global__ __launch_bounds__(256) void kv_write_kernel(const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
                                                       int64_t tokens, int kv_heads, const int64_t* __restrict__ slots,
                                                       int64_t num_blocks, const float* __restrict__ k_scale,
                                                       const float* __restrict__ v_scale, uint8_t* __restrict__ kc,
                                                       uint8_t* __restrict__ vc) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t per_token = (int64_t)kv_heads * (kDim / 8);
-  if (i >= tokens * per_token) return;
-  const int64_t t = i / per_token;
-  const int rem = (int)(i - t * per_token);
+  const int64_t per_quad = (int64_t)kv_heads * (kDim / 8);
+  const int64_t quads = (tokens + 3) / 4;
+  if (i >= quads * per_quad) return;
+  const int64_t tq = i / per_quad;
+  const int rem = (int)(i - tq * per_quad);
   const int h = rem / (kDim / 8), c = rem % (kDim / 8);
-  const int64_t slot = slots[t];
-  if (slot < 0 || slot >= num_blocks * kPage) return;
-  const int64_t blk = slot / kPage, off = slot % kPage;
-  const int64_t src = (t * kv_heads + h) * kDim + c * 8;
-  const int64_t page = (blk * kv_heads + h) * kPage * kDim;
-  const uint4 xk = *reinterpret_cast<const uint4*>(k + src);
-  const uint4 xv = *reinterpret_cast<const uint4*>(v + src);
+  const int64_t t0 = tq * 4;
+  const int nt = (int)min((int64_t)4, tokens - t0);
+  const int64_t limit = num_blocks * kPage;
   const float sk = k_scale[0], sv = v_scale[0];
-  *reinterpret_cast<uint2*>(kc + page + off * kDim + c * 8) =
-      make_uint2(quant4_static(xk.x, xk.y, sk), quant4_static(xk.z, xk.w, sk));
-  // values: byte (off / 4, dim, off % 4) of the page, dims c*8 .. c*8+7
-  const uint32_t v0 = quant4_static(xv.x, xv.y, sv), v1 = quant4_static(xv.z, xv.w, sv);
-  uint8_t* vd = vc + page + ((off >> 2) * kDim + c * 8) * 4 + (off & 3);
+  int64_t slot[4];
+  uint32_t vlo[4] = {0u, 0u, 0u, 0u}, vhi[4] = {0u, 0u, 0u, 0u};   // value codes of dims c*8 .. +3, +4 .. +7
 #pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    vd[4 * d] = (uint8_t)(v0 >> (8 * d));
-    vd[4 * (d + 4)] = (uint8_t)(v1 >> (8 * d));
+  for (int r = 0; r < 4; ++r) {
+    slot[r] = r < nt ? slots[t0 + r] : -1;
+    if (r < nt) {
+      const int64_t src = ((t0 + r) * kv_heads + h) * kDim + c * 8;
+      const uint4 xk = *reinterpret_cast<const uint4*>(k + src);
+      const uint4 xv = *reinterpret_cast<const uint4*>(v + src);
+      vlo[r] = quant4_static(xv.x, xv.y, sv);
+      vhi[r] = quant4_static(xv.z, xv.w, sv);
+      if (slot[r] >= 0 && slot[r] < limit) {
+        const int64_t blk = slot[r] / kPage, off = slot[r] % kPage;
+        *reinterpret_cast<uint2*>(kc + ((blk * kv_heads + h) * kPage + off) * kDim + c * 8) =
+            make_uint2(quant4_static(xk.x, xk.y, sk), quant4_static(xk.z, xk.w, sk));
+      }
+    }
+  }
+  const bool packed = nt == 4 && slot[0] >= 0 && slot[0] + 3 < limit && (slot[0] & 3) == 0 &&
+                      slot[1] == slot[0] + 1 && slot[2] == slot[0] + 2 && slot[3] == slot[0] + 3;
+  if (packed) {
+    // dword of dim d = the four tokens' codes of d, dims c*8 .. c*8+7 contiguous
+    const int64_t blk = slot[0] / kPage, off = slot[0] % kPage;
+    uint4* vd = reinterpret_cast<uint4*>(vc + ((blk * kv_heads + h) * kPage * kDim) + ((off >> 2) * kDim + c * 8) * 4);
+    vd[0] = make_uint4(gather_byte(vlo, 0), gather_byte(vlo, 1), gather_byte(vlo, 2), gather_byte(vlo, 3));
+    vd[1] = make_uint4(gather_byte(vhi, 0), gather_byte(vhi, 1), gather_byte(vhi, 2), gather_byte(vhi, 3));
+    return;
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (r >= nt || slot[r] < 0 || slot[r] >= limit) continue;
+    // values: byte (off / 4, dim, off % 4) of the page
+    const int64_t blk = slot[r] / kPage, off = slot[r] % kPage;
+    uint8_t* vd = vc + (blk * kv_heads + h) * kPage * kDim + ((off >> 2) * kDim + c * 8) * 4 + (off & 3);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      vd[4 * d] = (uint8_t)(vlo[r] >> (8 * d));
+      vd[4 * (d + 4)] = (uint8_t)(vhi[r] >> (8 * d));
+    }
   }
 }
 
@@ -387,7 +424,7 @@ hipError_t launch_kv_calibrate_scale(const uint16_t* x, int64_t n, float* scale,
 hipError_t launch_kv_cache_write(const uint16_t* k, const uint16_t* v, int64_t tokens, int kv_heads,
                                  const int64_t* slots, int64_t num_blocks, const float* k_scale, const float* v_scale,
                                  uint8_t* k_cache, uint8_t* v_cache, hipStream_t stream) {
-  const int64_t threads = tokens * kv_heads * (kDim / 8);
+  const int64_t threads = (tokens + 3) / 4 * kv_heads * (kDim / 8);
   hipLaunchKernelGGL(kv_write_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream, k, v, tokens,
                      kv_heads, slots, num_blocks, k_scale, v_scale, k_cache, v_cache);
   return hipGetLastError();

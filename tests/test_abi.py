@@ -224,6 +224,76 @@ def test_tis_argument_errors(lib):
     assert f(A16, A16, None, 1000, 2.0, A16, A16, A16 + 4, ws, None) == MISALIGNED
 
 
+def test_kv_calibrate_argument_errors(lib):
+    size = lib.fp8rl_kv_calibrate_workspace_size
+    f = lib.fp8rl_kv_calibrate_scale
+    assert size(-1) == 0 and size(0) == 4 and size(100000) == 49 * 4 and size(1 << 40) == 1024 * 4
+    ws = size(100000)
+    #        x    n       scale ws   bytes
+    assert f(A16, -1, A16, A16, ws, None) == INVALID
+    assert f(None, 100000, A16, A16, ws, None) == INVALID
+    assert f(A16, 100000, None, A16, ws, None) == INVALID
+    assert f(A16, 100000, A16, None, ws, None) == INVALID
+    assert f(A16, 100000, A16, A16, ws - 4, None) == INVALID                  # short workspace
+    assert f(A16, 1 << 46, A16, A16, 1 << 20, None) == SHAPE
+    assert f(A16 + 8, 100000, A16, A16, ws, None) == MISALIGNED               # 16-byte loads
+    assert f(A16, 100000, A16 + 2, A16, ws, None) == MISALIGNED
+    assert f(A16, 100000, A16, A16 + 2, ws, None) == MISALIGNED
+
+
+def test_kv_cache_write_argument_errors(lib):
+    f = lib.fp8rl_kv_cache_write_fp8
+    #        k    v    T   kvh hd   slots nb  ks   vs   kc   vc
+    assert f(A16, A16, -1, 8, 128, A16, 40, A16, A16, A16, A16, None) == INVALID
+    assert f(A16, A16, 300, 0, 128, A16, 40, A16, A16, A16, A16, None) == INVALID
+    assert f(A16, A16, 300, 8, 128, A16, -1, A16, A16, A16, A16, None) == INVALID
+    assert f(A16, A16, 300, 8, 64, A16, 40, A16, A16, A16, A16, None) == SHAPE        # head_dim 128 only
+    assert f(A16, A16, 300, 1025, 128, A16, 40, A16, A16, A16, A16, None) == SHAPE
+    assert f(A16, A16, 1 << 31, 8, 128, A16, 40, A16, A16, A16, A16, None) == SHAPE
+    assert f(A16, A16, 1 << 27, 1024, 128, A16, 40, A16, A16, A16, A16, None) == SHAPE  # grid of 2^31 threads
+    assert f(A16, A16, 300, 8, 128, None, 40, A16, A16, A16, A16, None) == INVALID
+    assert f(A16, A16, 300, 8, 128, A16, 40, A16, None, A16, A16, None) == INVALID
+    assert f(A16 + 8, A16, 300, 8, 128, A16, 40, A16, A16, A16, A16, None) == MISALIGNED
+    assert f(A16, A16, 300, 8, 128, A16 + 4, 40, A16, A16, A16, A16, None) == MISALIGNED
+    assert f(A16, A16, 300, 8, 128, A16, 40, A16, A16, A16, A16 + 4, None) == MISALIGNED
+    assert f(None, None, 0, 8, 128, None, 40, None, None, None, None, None) == OK      # no tokens: no-op
+
+
+def test_attention_decode_argument_errors(lib):
+    size = lib.fp8rl_attention_decode_workspace_size
+    assert size(2, 8, 2, 100) > 0
+    assert size(-1, 8, 2, 100) == 0 and size(2, 8, 3, 100) == 0 and size(2, 1, 2, 100) == 0 and size(2, 8, 2, -1) == 0
+    ws = size(2, 8, 2, 100)
+    f = lib.fp8rl_attention_decode_fp8kv
+    g = lib.fp8rl_attention_decode_bf16kv
+
+    def call(batch=2, qh=8, kvh=2, hd=128, nb=10, max_blocks=8, max_seq=100, ks=A16, sm=0.088, q=A16, wsb=ws,
+             table=A16, out=A16):
+        #        q  kc   vc   nb  table max_blocks seq_lens batch qh kvh hd max_seq ks vs sm out ws bytes
+        return f(q, A16, A16, nb, table, max_blocks, A16, batch, qh, kvh, hd, max_seq, ks, A16, sm, out, A16, wsb,
+                 None)
+
+    assert call(batch=-1) == INVALID
+    assert call(sm=0.0) == INVALID and call(sm=float("nan")) == INVALID and call(sm=float("inf")) == INVALID
+    assert call(hd=64) == SHAPE
+    assert call(qh=12, kvh=4) == SHAPE                    # group of 3
+    assert call(qh=32, kvh=2) == SHAPE                    # group of 16
+    assert call(qh=6, kvh=4) == SHAPE                     # not a multiple
+    assert call(batch=65536) == SHAPE
+    assert call(max_seq=1 << 30) == SHAPE
+    assert call(ks=None) == INVALID                       # FP8 cache needs its scales
+    assert call(table=None) == INVALID and call(out=None) == INVALID
+    assert call(nb=0) == INVALID
+    assert call(max_blocks=6) == INVALID                  # 6 * 16 < 100
+    assert call(wsb=ws - 16) == INVALID
+    assert call(q=A16 + 8) == MISALIGNED
+    assert call(out=A16 + 2) == MISALIGNED
+    assert call(batch=0, q=None, table=None, out=None) == OK
+    #        q    kc   vc   nb  table max_b seq  batch qh kvh hd   max_seq sm   out  ws   bytes
+    assert g(A16, A16, A16, 10, A16, 8, A16, 2, 8, 2, 64, 100, 0.088, A16, A16, ws, None) == SHAPE
+    assert g(A16, A16, A16, 10, A16, 8, A16, 2, 8, 2, 128, 100, 0.088, A16, None, ws, None) == INVALID
+
+
 def test_binding_rejects_cpu_tensors():
     import torch
     import paper_2601_18150_amd as fp8rl

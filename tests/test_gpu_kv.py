@@ -75,6 +75,49 @@ def test_cache_write_bit_exact_with_saturation_and_padding(fp8rl):
     assert_codes_equal(u8(vc), vc_ref, "v cache")
 
 
+def prefill_slots(rng, nb, runs):
+    """Token slots of several prefill runs, each (start offset in its first block, tokens),
+    over shuffled blocks; padding (-1), an out-of-range slot and a reversed pair mixed in."""
+    blocks = list(rng.permutation(nb))
+    out = []
+    for start, n in runs:
+        need = (start + n + 15) // 16
+        own, blocks = blocks[:need], blocks[need:]
+        out += [int(own[(start + t) // 16]) * 16 + (start + t) % 16 for t in range(n)]
+    out = np.array(out, np.int64)
+    return out
+
+
+@pytest.mark.parametrize("runs", [[(0, 64)], [(0, 37), (5, 29), (0, 16), (12, 9), (3, 1)], [(2, 81), (0, 3)]])
+def test_cache_write_prefill_runs_bit_exact(fp8rl, runs):
+    """Tokens of whole prefills in order (four tokens to four consecutive slots from a
+    multiple of 4: whole value dwords) mixed with runs that start mid-dword, ragged
+    ends, padding inside a run, a slot past the cache and a swapped pair."""
+    announce(f"kv cache write: prefill runs {runs}")
+    rng = np.random.default_rng(len(runs))
+    kvh, nb = 4, 24
+    slots = prefill_slots(rng, nb, runs)
+    t = len(slots)
+    if t > 20:
+        slots[13] = -1                      # padding inside a run
+        slots[18] = nb * 16 + 3             # past the cache: skipped
+        slots[[8, 9]] = slots[[9, 8]]       # swapped pair
+    k = bf16(rng, (t, kvh, 128))
+    v = bf16(rng, (t, kvh, 128), 0.5)
+    ks, vs = np.float32(3.0 / 448), np.float32(1.5 / 448)
+    kc = torch.full((nb, kvh, 16, 128), 0xCD, dtype=torch.uint8, device="cuda")
+    vc = torch.full((nb, kvh, 4, 128, 4), 0xCD, dtype=torch.uint8, device="cuda")
+    fp8rl.fp8rl_kv_cache_write_fp8(k.cuda(), v.cuda(), torch.from_numpy(slots).cuda(),
+                                   torch.tensor([ks]).cuda(), torch.tensor([vs]).cuda(), kc, vc)
+    torch.cuda.synchronize()
+    kc_ref = np.full((nb, kvh, 16, 128), 0xCD, np.uint8)
+    vc_ref = np.full((nb, kvh, 4, 128, 4), 0xCD, np.uint8)
+    keep = (slots >= 0) & (slots < nb * 16)
+    kv.write_cache(kc_ref, vc_ref, u16(k)[keep], u16(v)[keep], slots[keep], ks, vs)
+    assert_codes_equal(u8(kc), kc_ref, "k cache")
+    assert_codes_equal(u8(vc), vc_ref, "v cache")
+
+
 def paged_inputs(rng, seq_lens, q_heads, kv_heads, spare=5, bf16_cache=False):
     pages = [(int(n) + 15) // 16 for n in seq_lens]
     nb = sum(pages) + spare
