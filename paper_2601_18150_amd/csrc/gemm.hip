@@ -10,13 +10,19 @@
 namespace fp8rl {
 namespace {
 
-// Tile configurations.
-// (measured on MI355X: 256x128 tiles with 3 slots and 128x128 tiles with 3
-// slots were both slower than these two on every configured shape; 128x128
-// with 2 slots fits two workgroups per CU, which is what small-M and MoE
-// shapes need to fill the 256 CUs)
+// Tile configurations (BN x BM, waves, LDS ring depth), measured on MI355X:
+// - M and N >= 2048: 256x256, 8 waves, 2 slots (one workgroup per CU).
+// - other M > 256, and the grouped GEMM: 128x128, 4 waves, 2 slots: two
+//   workgroups per CU walking their tiles as one pipeline.  Deeper rings with
+//   one workgroup per CU were slower here (MoE gate_up 270 vs 205 us).
+// - 128 < M <= 256 (decode batches): one 256-token tile, 128x256, 8 waves, 3
+//   slots (Qwen3-8B gate_up at M = 256: 44.8 vs 48.0 us).
+// - split-K ranges: 128x128, 3 slots (decode linears 123 vs 129 us per layer).
 using CfgLarge = GemmCfg<256, 256, 2, 4, 2>;   // 512 threads, wave tile 128(n) x 64(m), 130 KiB LDS
 using CfgSmall = GemmCfg<128, 128, 2, 2, 2>;   // 256 threads, wave tile 64 x 64, 65 KiB LDS
+using CfgDecode = GemmCfg<128, 256, 2, 4, 3>;  // 512 threads, wave tile 64 x 64, 147 KiB LDS
+using CfgSplitK = GemmCfg<128, 128, 2, 2, 3>;  // one tile per workgroup, 2 K steps in flight, 98 KiB LDS
+using CfgGrouped = CfgSmall;
 
 constexpr int kXcds = 8;        // MI355X: workgroup i is dispatched to XCD i % 8
 constexpr int kGroupM = 8;      // m tiles per band of the grouped raster order
@@ -53,7 +59,7 @@ __device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n
 // step) for the 128x128 tiles; the 256x256 tile has no registers to spare for
 // the next tile's load plan and runs one tile per workgroup.
 template <class C>
-constexpr bool kCrossTiles = C::BN * C::BM <= 128 * 128;
+constexpr bool kCrossTiles = C::BN * C::BM <= 128 * 128 && C::STAGES == 2;
 
 // Job providers for gemm_tiles (see gemm_core.hpp): wave-uniform, no LDS
 // writes, no synchronisation.
@@ -285,11 +291,14 @@ hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* s
                                   const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y, int64_t ldy,
                                   int64_t m, int64_t n, int64_t k, hipStream_t stream, bool pow2_scales) {
   const bool large = m >= 2048 && n >= 2048;
+  const bool decode = !large && m > 128 && m <= 256;
   if (pow2_scales)
-    return large ? launch_dense<CfgLarge, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
-                 : launch_dense<CfgSmall, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
-  return large ? launch_dense<CfgLarge, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
-               : launch_dense<CfgSmall, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+    return large    ? launch_dense<CfgLarge, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+           : decode ? launch_dense<CfgDecode, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+                    : launch_dense<CfgSmall, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
+  return large    ? launch_dense<CfgLarge, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+         : decode ? launch_dense<CfgDecode, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+                  : launch_dense<CfgSmall, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
 }
 
 int splitk_factor(int64_t m, int64_t n, int64_t k) {
@@ -313,7 +322,7 @@ hipError_t launch_gemm_w8a8_block_splitk(const uint8_t* qa, int64_t lda, const f
                                          const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y,
                                          int64_t ldy, int64_t m, int64_t n, int64_t k, float* part, int splits,
                                          hipStream_t stream) {
-  using C = CfgSmall;
+  using C = CfgSplitK;
   const int tiles_m = (int)((m + C::BM - 1) / C::BM);
   const int tiles_n = (int)(n / C::BN);
   hipLaunchKernelGGL(gemm_w8a8_block_splitk_kernel<C>, dim3((unsigned)(tiles_m * tiles_n * splits)),
@@ -332,10 +341,10 @@ hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, in
                                           int64_t num_groups, int64_t total_rows, uint16_t* y, int64_t n,
                                           int64_t k, hipStream_t stream, bool pow2_scales) {
   if (pow2_scales)
-    return launch_grouped<CfgSmall, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
-                                          stream);
-  return launch_grouped<CfgSmall, false>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
-                                         stream);
+    return launch_grouped<CfgGrouped, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n,
+                                            k, stream);
+  return launch_grouped<CfgGrouped, false>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
+                                           stream);
 }
 
 }  // namespace fp8rl

@@ -34,13 +34,14 @@ namespace fp8rl {
 typedef int v8i32 __attribute__((ext_vector_type(8)));
 typedef float v4f32 __attribute__((ext_vector_type(4)));
 
-template <int BN_, int BM_, int WN_, int WM_, int STAGES_>
+template <int BN_, int BM_, int WN_, int WM_, int STAGES_, int WPOL_ = 0, int DMAW_ = 0>
 struct GemmCfg {
   static constexpr int BN = BN_;            // tile extent along n (weight rows)
   static constexpr int BM = BM_;            // tile extent along m (tokens)
   static constexpr int WN = WN_;            // waves along n
   static constexpr int WM = WM_;            // waves along m
   static constexpr int STAGES = STAGES_;    // LDS ring depth (K steps in flight)
+  static constexpr int kWPolicy = WPOL_;    // cache-policy bits of the weight-tile DMA (0: default)
   static constexpr int kWaves = WN * WM;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int WTN = BN / WN;       // wave tile along n
@@ -54,13 +55,16 @@ struct GemmCfg {
   static constexpr int kLdsBytes = STAGES * kStageBytes;
   // one direct-to-LDS wave instruction moves 8 rows x 128 bytes (1 KiB)
   static constexpr int kOctets = (BN + BM) / 8;
-  static constexpr int kLoadsPerWave = kOctets / kWaves;
+  // waves that issue the DMA (the first kDmaWaves; 0 in the template: all)
+  static constexpr int kDmaWaves = DMAW_ ? DMAW_ : kWaves;
+  static constexpr int kLoadsPerWave = kOctets / kDmaWaves;
   // activation scales: 64 tokens (one dword each) per wave instruction
   static constexpr int kScaleLoads = BM / 64;
   static_assert(BM % 64 == 0 && kScaleLoads <= kWaves, "one scale DMA per wave at most");
   static_assert(WTN % 16 == 0 && WTM % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(WTN <= 128 && 128 % WTN == 0, "a wave's n range must sit inside one 128-row scale block");
-  static_assert(kOctets % kWaves == 0, "row octets must divide evenly among the waves");
+  static_assert(kOctets % kDmaWaves == 0 && kDmaWaves <= kWaves, "row octets must divide evenly among the DMA waves");
+  static_assert(kScaleLoads <= kDmaWaves, "scale DMA waves must be DMA waves");
   static_assert(STAGES >= 2, "need at least double buffering");
   static_assert(kLdsBytes <= 160 * 1024, "LDS is 160 KiB per CU");
 };
@@ -99,8 +103,9 @@ typedef __attribute__((address_space(1))) const void global_void_t;
 // 16 bytes per lane, global -> LDS without passing through registers
 // (global_load_lds_dwordx4): lane L of the wave writes LDS bytes
 // [lds_wave_base + 16 L, +16).  lds_wave_base must be wave-uniform.
+template <int kPol = 0>
 __device__ __forceinline__ void lds_dma16(const uint8_t* gptr, uint8_t* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 16, 0, 0);
+  __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 16, 0, kPol);
 }
 
 // 4 bytes per lane, global -> LDS (global_load_lds_dword): lane L writes
@@ -120,9 +125,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) 
 // address = base + voff + soff, with a 32-bit per-lane offset (one VGPR) and a
 // wave-uniform one (an SGPR).  Used in the K loop, where the 64-bit per-lane
 // addresses of global_load_lds would hold two VGPRs per load.
+template <int kPol = 0>
 __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
                                           uint8_t* lds_wave_base) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_wave_base, 16, voff, soff, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_wave_base, 16, voff, soff, 0, kPol);
 }
 
 // 16-byte streaming (non-temporal) store of eight bf16
@@ -151,6 +157,22 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// At the top of a K step with `later` further steps' DMA already issued behind
+// it (kPer wave instructions each), wait until this step's DMA has landed.
+// Loads complete in issue order, so vmcnt(later * kPer) suffices; the count
+// must be an immediate, hence the branches (later <= S - 2).
+template <int S, int kPer>
+__device__ __forceinline__ void wait_dma_step(int later) {
+  static_assert(S >= 2 && S <= 4, "ring depth 2..4");
+  if constexpr (S == 2) {
+    wait_vmcnt<0>();
+  } else if constexpr (S == 3) {
+    if (later >= 1) wait_vmcnt<kPer>(); else wait_vmcnt<0>();
+  } else {
+    if (later >= 2) wait_vmcnt<2 * kPer>(); else if (later == 1) wait_vmcnt<kPer>(); else wait_vmcnt<0>();
+  }
+}
+
 // One output tile to compute (wave-uniform values, produced by a job provider).
 struct TileJob {
   int row_lo;              // first row of A / Y
@@ -172,17 +194,18 @@ struct TileJob {
 // 128 weight rows) are sw_ld floats apart.  kPartial: write the fp32 sums to part (rows of
 // N floats) instead of bf16 to y (one K range of a split-K product).
 //
-// Pipeline (2-slot LDS ring, one barrier per K step):
+// Pipeline (S-slot LDS ring, S = C::STAGES, one barrier per K step):
+//   prologue: the DMA of steps 0 .. S-2 into slots 0 .. S-2.
 //   step s:  wait for this wave's DMA of step s; barrier (all waves' DMA of step
 //            s landed, all waves done reading step s-1's slot); MFMA + scale-FMA
-//            on slot s % 2, with the DMA of step s+1 into the other slot
-//            interleaved.
-//   kCross:  after a tile's last K block, step s+1 is the first K block of the
-//            workgroup's next tile, so consecutive tiles form one pipeline and
-//            the next tile's first load overlaps this tile's last step and
-//            output.  Without it the workgroup computes its first tile only
-//            (the 256x256 tile, whose registers are full, runs one tile per
-//            workgroup).
+//            on slot s % S, with the DMA of step s+S-1 into the slot of step s-1
+//            interleaved.  S - 1 K steps are in flight while one is computed.
+//   kCross (2-slot ring only): after a tile's last K block, step s+1 is the
+//            first K block of the workgroup's next tile, so consecutive tiles
+//            form one pipeline and the next tile's first load overlaps this
+//            tile's last step and output.  Without it the workgroup computes its
+//            first tile only (the 256x256 tile, whose registers are full, runs
+//            one tile per workgroup).
 //   tile end: the bf16 tile is staged through the slot of its last step (in
 //            row groups that fit one slot) and written as whole output rows.
 // A slot holds the W tile, the A tile and the tile's BM activation scales of
@@ -197,7 +220,8 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
                                            const float* __restrict__ sw, int sw_ld,
                                            uint16_t* __restrict__ y, int64_t ldy, float* __restrict__ part,
                                            int N, int KB, Jobs& jobs, uint8_t* lds) {
-  static_assert(C::STAGES == 2, "the tile pipeline is written for a 2-slot ring");
+  constexpr int S = C::STAGES;
+  static_assert(S == 2 || !kCross, "the cross-tile pipeline is written for a 2-slot ring");
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -218,7 +242,7 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
   auto dma_offsets = [&](uint32_t (&g)[C::kLoadsPerWave], int n_valid, int m_valid) {
 #pragma unroll
     for (int i = 0; i < C::kLoadsPerWave; ++i) {
-      const int o = wave + i * C::kWaves;               // wave-uniform
+      const int o = wave + i * C::kDmaWaves;            // wave-uniform
       const bool w = o < C::BN / 8;
       const int r = (w ? o : o - C::BN / 8) * 8 + lrow;
       const int lchunk = (lane & 7) ^ swz_key(r);
@@ -230,6 +254,7 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
   // to the last valid row); this wave's 128-row weight scale block is read with
   // scalar loads (a wave past N reads the last block and stores nothing)
   const bool sdma = wave < C::kScaleLoads;
+  const bool dma_wave = wave < C::kDmaWaves;
   auto n_valid_of = [&](const TileJob& j) { return min(C::BN, N - j.n0); };
   auto sa_lane_of = [&](const TileJob& j) { return sa + j.row_lo + min(wave * 64 + lane, j.m_valid - 1); };
 
@@ -244,16 +269,25 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
     if (has_nxt) dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid);
   }
 
-  // prologue: the first tile's first K block into slot 0
-  {
-    const uint8_t* wb = qw + cur.qw_off + (int64_t)cur.n0 * ldw;
-    const uint8_t* ab = qa + (int64_t)cur.row_lo * lda;
+  // prologue: the first tile's first S-1 K blocks into slots 0 .. S-2
+#pragma unroll
+  for (int p = 0; p < S - 1; ++p) {
+    if (p > 0 && p >= KB) break;
+    const uint8_t* wb = qw + cur.qw_off + (int64_t)cur.n0 * ldw + p * 128;
+    const uint8_t* ab = qa + (int64_t)cur.row_lo * lda + p * 128;
+    uint8_t* ps = lds + p * C::kStageBytes;
 #pragma unroll
     for (int i = 0; i < C::kLoadsPerWave; ++i) {
-      const int o = wave + i * C::kWaves;
-      lds_dma16((o < C::BN / 8 ? wb : ab) + goff[i], lds + o * 1024);
+      if (!dma_wave) break;
+      const int o = wave + i * C::kDmaWaves;
+      if constexpr (C::kWPolicy == 0) {
+        lds_dma16((o < C::BN / 8 ? wb : ab) + goff[i], ps + o * 1024);
+      } else {
+        if (o < C::BN / 8) lds_dma16<C::kWPolicy>(wb + goff[i], ps + o * 1024);
+        else lds_dma16(ab + goff[i], ps + o * 1024);
+      }
     }
-    if (sdma) lds_dma4(sa_lane_of(cur), lds + C::kWBytes + C::kABytes + wave * 256);
+    if (sdma) lds_dma4(sa_lane_of(cur) + (int64_t)p * ld_sa, ps + C::kWBytes + C::kABytes + wave * 256);
   }
 
   int slot = 0;
@@ -271,7 +305,11 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       for (int j = 0; j < C::TM; ++j) acc[i][j] = (v4f32){0.f, 0.f, 0.f, 0.f};
 
     for (int kb = 0; kb < KB; ++kb) {
-      wait_vmcnt<0>();        // this step's DMA (and a previous tile's output stores)
+      // this step's DMA (with S = 2 also a previous tile's output stores)
+      const int later = min(S - 2, KB - 1 - kb);
+      if (sdma) wait_dma_step<S, C::kLoadsPerWave + 1>(later);
+      else if (dma_wave) wait_dma_step<S, C::kLoadsPerWave>(later);
+      else wait_vmcnt<0>();
       lds_barrier();
 
       // refill the other slot with the next step: the next K block of this tile
@@ -282,12 +320,12 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       // barrier); with fewer, all are issued with the first one (measured
       // fastest for the 128x128 tiles).
       const bool last = kb + 1 == KB;
-      const bool refill = !last || has_nxt;
-      uint8_t* dslot = lds + (slot ^ 1) * C::kStageBytes;
+      const bool refill = kb + S - 1 < KB || (last && has_nxt);
+      uint8_t* dslot = lds + (slot == 0 ? S - 1 : slot - 1) * C::kStageBytes;
       const uint8_t* dwb = wbase;
       const uint8_t* dab = abase;
-      uint32_t dsoff = (kb + 1) * 128;
-      const float* dsa = sa_lane + (int64_t)(kb + 1) * ld_sa;
+      uint32_t dsoff = (kb + S - 1) * 128;
+      const float* dsa = sa_lane + (int64_t)(kb + S - 1) * ld_sa;
       if constexpr (kCross) {
         if (last) {
           dwb = qw + nxt.qw_off + (int64_t)nxt.n0 * ldw;
@@ -330,11 +368,16 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       for (int tn = 0; tn < C::TN; ++tn) {
 #pragma unroll
         for (int i = 0; i < C::kLoadsPerWave; ++i) {
-          if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill) {
-            const int o = wave + i * C::kWaves;
+          if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill && dma_wave) {
+            const int o = wave + i * C::kDmaWaves;
             uint32_t off = goff[i];
             if constexpr (kCross) off = last ? goff_n[i] : goff[i];
-            lds_dma16(o < C::BN / 8 ? rw : ra, off, dsoff, dslot + o * 1024);
+            if constexpr (C::kWPolicy == 0) {
+              lds_dma16(o < C::BN / 8 ? rw : ra, off, dsoff, dslot + o * 1024);
+            } else {
+              if (o < C::BN / 8) lds_dma16<C::kWPolicy>(rw, off, dsoff, dslot + o * 1024);
+              else lds_dma16(ra, off, dsoff, dslot + o * 1024);
+            }
           }
         }
         if (tn == 0 && sdma && refill) lds_dma4(dsa, dslot + C::kWBytes + C::kABytes + wave * 256);
@@ -361,12 +404,13 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
         }
         af = af_next;
       }
-      slot ^= 1;
+      slot = slot + 1 == S ? 0 : slot + 1;
     }
 
-    // ---- tile end.  The slot of the last K step (slot ^ 1 now) is free once
-    //      every wave is past the barrier below; with kCross the other holds
-    //      the next tile's first K block (in flight).
+    // ---- tile end.  The slot of the last K step (slot ^ 1 now; kCross, so
+    //      S = 2) is free once every wave is past the barrier below; with kCross
+    //      the other holds the next tile's first K block (in flight).  Without
+    //      kCross no DMA is in flight and the whole ring is free.
     if constexpr (kPartial) {
       // split-K partial: the fp32 sums, four consecutive n per lane (16 bytes)
 #pragma unroll

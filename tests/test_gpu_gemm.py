@@ -104,6 +104,8 @@ def quantised_operands(m, n, k, seed):
     (37, 384, 256, (16, 8, 3)),
     (100, 256, 512, (0, 0, 0)),
     (129, 640, 384, (32, 24, 1)),
+    (200, 1152, 1280, (16, 8, 2)),
+    (256, 256, 128, (0, 0, 0)),
     (300, 512, 256, (0, 0, 0)),
     (2048, 2048, 256, (0, 0, 0)),
     (2100, 2176, 384, (16, 8, 5)),
