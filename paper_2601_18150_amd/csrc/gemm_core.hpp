@@ -34,14 +34,13 @@ namespace fp8rl {
 typedef int v8i32 __attribute__((ext_vector_type(8)));
 typedef float v4f32 __attribute__((ext_vector_type(4)));
 
-template <int BN_, int BM_, int WN_, int WM_, int STAGES_, int WPOL_ = 0, int DMAW_ = 0>
+template <int BN_, int BM_, int WN_, int WM_, int STAGES_>
 struct GemmCfg {
   static constexpr int BN = BN_;            // tile extent along n (weight rows)
   static constexpr int BM = BM_;            // tile extent along m (tokens)
   static constexpr int WN = WN_;            // waves along n
   static constexpr int WM = WM_;            // waves along m
   static constexpr int STAGES = STAGES_;    // LDS ring depth (K steps in flight)
-  static constexpr int kWPolicy = WPOL_;    // cache-policy bits of the weight-tile DMA (0: default)
   static constexpr int kWaves = WN * WM;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int WTN = BN / WN;       // wave tile along n
@@ -55,16 +54,13 @@ struct GemmCfg {
   static constexpr int kLdsBytes = STAGES * kStageBytes;
   // one direct-to-LDS wave instruction moves 8 rows x 128 bytes (1 KiB)
   static constexpr int kOctets = (BN + BM) / 8;
-  // waves that issue the DMA (the first kDmaWaves; 0 in the template: all)
-  static constexpr int kDmaWaves = DMAW_ ? DMAW_ : kWaves;
-  static constexpr int kLoadsPerWave = kOctets / kDmaWaves;
+  static constexpr int kLoadsPerWave = kOctets / kWaves;
   // activation scales: 64 tokens (one dword each) per wave instruction
   static constexpr int kScaleLoads = BM / 64;
   static_assert(BM % 64 == 0 && kScaleLoads <= kWaves, "one scale DMA per wave at most");
   static_assert(WTN % 16 == 0 && WTM % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(WTN <= 128 && 128 % WTN == 0, "a wave's n range must sit inside one 128-row scale block");
-  static_assert(kOctets % kDmaWaves == 0 && kDmaWaves <= kWaves, "row octets must divide evenly among the DMA waves");
-  static_assert(kScaleLoads <= kDmaWaves, "scale DMA waves must be DMA waves");
+  static_assert(kOctets % kWaves == 0, "row octets must divide evenly among the waves");
   static_assert(STAGES >= 2, "need at least double buffering");
   static_assert(kLdsBytes <= 160 * 1024, "LDS is 160 KiB per CU");
 };
@@ -103,9 +99,8 @@ typedef __attribute__((address_space(1))) const void global_void_t;
 // 16 bytes per lane, global -> LDS without passing through registers
 // (global_load_lds_dwordx4): lane L of the wave writes LDS bytes
 // [lds_wave_base + 16 L, +16).  lds_wave_base must be wave-uniform.
-template <int kPol = 0>
 __device__ __forceinline__ void lds_dma16(const uint8_t* gptr, uint8_t* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 16, 0, kPol);
+  __builtin_amdgcn_global_load_lds((global_void_t*)gptr, (lds_void_t*)lds_wave_base, 16, 0, 0);
 }
 
 // 4 bytes per lane, global -> LDS (global_load_lds_dword): lane L writes
@@ -125,10 +120,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base) 
 // address = base + voff + soff, with a 32-bit per-lane offset (one VGPR) and a
 // wave-uniform one (an SGPR).  Used in the K loop, where the 64-bit per-lane
 // addresses of global_load_lds would hold two VGPRs per load.
-template <int kPol = 0>
 __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
                                           uint8_t* lds_wave_base) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_wave_base, 16, voff, soff, 0, kPol);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)lds_wave_base, 16, voff, soff, 0, 0);
 }
 
 // 16-byte streaming (non-temporal) store of eight bf16
@@ -242,7 +236,7 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
   auto dma_offsets = [&](uint32_t (&g)[C::kLoadsPerWave], int n_valid, int m_valid) {
 #pragma unroll
     for (int i = 0; i < C::kLoadsPerWave; ++i) {
-      const int o = wave + i * C::kDmaWaves;            // wave-uniform
+      const int o = wave + i * C::kWaves;               // wave-uniform
       const bool w = o < C::BN / 8;
       const int r = (w ? o : o - C::BN / 8) * 8 + lrow;
       const int lchunk = (lane & 7) ^ swz_key(r);
@@ -254,7 +248,6 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
   // to the last valid row); this wave's 128-row weight scale block is read with
   // scalar loads (a wave past N reads the last block and stores nothing)
   const bool sdma = wave < C::kScaleLoads;
-  const bool dma_wave = wave < C::kDmaWaves;
   auto n_valid_of = [&](const TileJob& j) { return min(C::BN, N - j.n0); };
   auto sa_lane_of = [&](const TileJob& j) { return sa + j.row_lo + min(wave * 64 + lane, j.m_valid - 1); };
 
@@ -278,14 +271,8 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
     uint8_t* ps = lds + p * C::kStageBytes;
 #pragma unroll
     for (int i = 0; i < C::kLoadsPerWave; ++i) {
-      if (!dma_wave) break;
-      const int o = wave + i * C::kDmaWaves;
-      if constexpr (C::kWPolicy == 0) {
-        lds_dma16((o < C::BN / 8 ? wb : ab) + goff[i], ps + o * 1024);
-      } else {
-        if (o < C::BN / 8) lds_dma16<C::kWPolicy>(wb + goff[i], ps + o * 1024);
-        else lds_dma16(ab + goff[i], ps + o * 1024);
-      }
+      const int o = wave + i * C::kWaves;
+      lds_dma16((o < C::BN / 8 ? wb : ab) + goff[i], ps + o * 1024);
     }
     if (sdma) lds_dma4(sa_lane_of(cur) + (int64_t)p * ld_sa, ps + C::kWBytes + C::kABytes + wave * 256);
   }
@@ -308,12 +295,12 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       // this step's DMA (with S = 2 also a previous tile's output stores)
       const int later = min(S - 2, KB - 1 - kb);
       if (sdma) wait_dma_step<S, C::kLoadsPerWave + 1>(later);
-      else if (dma_wave) wait_dma_step<S, C::kLoadsPerWave>(later);
-      else wait_vmcnt<0>();
+      else wait_dma_step<S, C::kLoadsPerWave>(later);
       lds_barrier();
 
-      // refill the other slot with the next step: the next K block of this tile
-      // or, after its last, the first K block of the next tile (if any).  With 8
+      // refill the slot of step s-1 with step s+S-1: a later K block of this
+      // tile or, with kCross after its last, the first K block of the next tile
+      // (if any).  With 8
       // sub-tile rows per wave the DMA instructions are spread over the first
       // half of the sub-tile loop below (issued all at once they stall the wave
       // on a full address queue, issued later they arrive after the next
@@ -368,16 +355,11 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       for (int tn = 0; tn < C::TN; ++tn) {
 #pragma unroll
         for (int i = 0; i < C::kLoadsPerWave; ++i) {
-          if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill && dma_wave) {
-            const int o = wave + i * C::kDmaWaves;
+          if ((i * kDmaSpread) / C::kLoadsPerWave == tn && refill) {
+            const int o = wave + i * C::kWaves;
             uint32_t off = goff[i];
             if constexpr (kCross) off = last ? goff_n[i] : goff[i];
-            if constexpr (C::kWPolicy == 0) {
-              lds_dma16(o < C::BN / 8 ? rw : ra, off, dsoff, dslot + o * 1024);
-            } else {
-              if (o < C::BN / 8) lds_dma16<C::kWPolicy>(rw, off, dsoff, dslot + o * 1024);
-              else lds_dma16(ra, off, dsoff, dslot + o * 1024);
-            }
+            lds_dma16(o < C::BN / 8 ? rw : ra, off, dsoff, dslot + o * 1024);
           }
         }
         if (tn == 0 && sdma && refill) lds_dma4(dsa, dslot + C::kWBytes + C::kABytes + wave * 256);
