@@ -70,6 +70,35 @@ int fp8rl_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t
                                 uint8_t* q, int64_t ldq, float* scale, void* stream);
 
 /*
+ * Weight re-quantisation of many matrices in one pass.  After every RL step the
+ * trainer's updated bf16 weights are synced into the rollout engine and every
+ * quantised linear layer is re-quantised (section 2.1.2; section 2.1.1 Eq. (1)).
+ * For each jobs[i] this computes exactly what
+ *   fp8rl_quant_weight_block128(w, n, k, ldw, q, ldq, scale, stream)
+ * computes (same layouts, alignment and size rules, bit-identical codes and
+ * scales), with up to 64 matrices per kernel launch, so the memory pipeline stays
+ * full across matrices instead of ramping up and draining once per matrix.
+ *
+ * jobs   HOST array of `count` job descriptors, read during the call only; the
+ *        pointers inside are device pointers.  Jobs with n == 0 or k == 0 are
+ *        skipped.  No job's outputs may overlap another job's inputs or outputs.
+ * count  >= 0 (0 is a no-op); jobs may be NULL only when count == 0.
+ * Errors: every job is validated before anything is launched; the first invalid
+ * job's error code is returned (FP8RL_ERR_INVALID_ARG also for count < 0 or a
+ * NULL jobs array).  FP8RL_ERR_HIP after a launch failure: launches of earlier
+ * 64-job chunks may then have run.
+ */
+typedef struct fp8rl_weight_job {
+  const uint16_t* w;     /* [n][ldw] bf16 weight */
+  int64_t n, k, ldw;
+  uint8_t* q;            /* [n][ldq] E4M3 codes out */
+  int64_t ldq;
+  float* scale;          /* [n/128][k/128] fp32 block scales out */
+} fp8rl_weight_job;
+
+int fp8rl_quant_weight_block128_batched(const fp8rl_weight_job* jobs, int64_t count, void* stream);
+
+/*
  * Dynamic activation quantisation, one fp32 scale per token per 128-wide K group
  * (section 2.1.1 "Static vs dynamic quantization"; section 3.1 1x128 tiles).
  *

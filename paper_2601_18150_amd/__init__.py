@@ -21,7 +21,7 @@ import torch  # loads torch's HIP runtime first, so libfp8rl binds to that same 
 
 __all__ = [
     "LIB_PATH", "Fp8rlError", "load",
-    "fp8rl_quant_weight_block128", "fp8rl_quant_act_token_group128",
+    "fp8rl_quant_weight_block128", "fp8rl_quant_weight_block128_batched", "fp8rl_quant_act_token_group128",
     "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
     "fp8rl_gemm_w8a8_block_workspace_size", "fp8rl_gemm_w8a8_block_ws",
     "fp8rl_quant_weight_block128_ue8m0", "fp8rl_quant_act_token_group128_ue8m0",
@@ -84,6 +84,8 @@ def _load():
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = ctypes.c_int
+    lib.fp8rl_quant_weight_block128_batched.argtypes = [P, I, P]
+    lib.fp8rl_quant_weight_block128_batched.restype = ctypes.c_int
     lib.fp8rl_tis_workspace_size.argtypes = [I]
     lib.fp8rl_tis_workspace_size.restype = ctypes.c_int64
     lib.fp8rl_kv_calibrate_workspace_size.argtypes = [I]
@@ -167,6 +169,43 @@ def fp8rl_quant_weight_block128(w: torch.Tensor, q: torch.Tensor | None = None,
                                 scale: torch.Tensor | None = None, stream=None):
     """bf16 weight [N][K] -> (E4M3 codes uint8 [N][K], fp32 scales [N/128][K/128])."""
     return _quant_weight("fp8rl_quant_weight_block128", w, q, scale, stream)
+
+
+class WeightJob(ctypes.Structure):
+    """fp8rl_weight_job of include/fp8rl.h (device pointers, sizes in elements)."""
+    _fields_ = [("w", ctypes.c_void_p), ("n", ctypes.c_int64), ("k", ctypes.c_int64), ("ldw", ctypes.c_int64),
+                ("q", ctypes.c_void_p), ("ldq", ctypes.c_int64), ("scale", ctypes.c_void_p)]
+
+
+def fp8rl_quant_weight_block128_batched(ws, qs=None, scales=None, stream=None):
+    """Many bf16 weights [N_i][K_i] -> [(codes, scales)] in one pass (up to 64 matrices per launch);
+    each result is bit-identical to fp8rl_quant_weight_block128 of that matrix."""
+    ws = list(ws)
+    qs = list(qs) if qs is not None else [None] * len(ws)
+    scales = list(scales) if scales is not None else [None] * len(ws)
+    if len(qs) != len(ws) or len(scales) != len(ws):
+        raise ValueError("ws, qs and scales must have the same length")
+    jobs = (WeightJob * max(len(ws), 1))()
+    out = []
+    for i, (w, q, sc) in enumerate(zip(ws, qs, scales)):
+        if w.dtype != torch.bfloat16 or w.dim() != 2:
+            raise TypeError("every w must be a 2-D bfloat16 tensor")
+        n, k = w.shape
+        if q is None:
+            q = torch.empty((n, k), dtype=torch.uint8, device=w.device)
+        if sc is None:
+            sc = torch.empty((n // 128, k // 128), dtype=torch.float32, device=w.device)
+        q = _u8(q)
+        _dev(w, q, sc)
+        if sc.dtype != torch.float32 or not sc.is_contiguous() or sc.numel() < (n // 128) * (k // 128):
+            raise ValueError("scale must be a contiguous fp32 tensor of [N/128][K/128] elements")
+        jobs[i] = WeightJob(w.data_ptr(), n, k, _ld(w), q.data_ptr(), _ld(q), sc.data_ptr())
+        out.append((q, sc))
+    if ws:
+        _dev(*ws)
+    st = load().fp8rl_quant_weight_block128_batched(ctypes.addressof(jobs), len(ws), _stream(stream))
+    _check("fp8rl_quant_weight_block128_batched", st)
+    return out
 
 
 def fp8rl_quant_weight_block128_ue8m0(w: torch.Tensor, q: torch.Tensor | None = None,

@@ -56,8 +56,9 @@ const char* fp8rl_status_string(int status) {
 
 int fp8rl_version(void) { return 100; }   // 0.1.0
 
-static int quant_weight(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q, int64_t ldq,
-                        float* scale, void* stream, bool pow2) {
+// Validation of one weight matrix: an FP8RL_* error, FP8RL_OK (nothing to do) or kLaunch.
+static int check_weight(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, const uint8_t* q, int64_t ldq,
+                        const float* scale) {
   if (n < 0 || k < 0) return FP8RL_ERR_INVALID_ARG;
   if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
   if (n >= kMaxDim || k >= kMaxDim || (n / 128) * (k / 128) >= (int64_t(1) << 24))
@@ -67,7 +68,34 @@ static int quant_weight(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, ui
   if (ldw < k || ldq < k) return FP8RL_ERR_INVALID_ARG;
   if (!aligned(w, 16) || !aligned(q, 16) || !aligned(scale, 4) || ldw % 8 || ldq % 16)
     return FP8RL_ERR_MISALIGNED;
+  return kLaunch;
+}
+
+static int quant_weight(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q, int64_t ldq,
+                        float* scale, void* stream, bool pow2) {
+  const int st = check_weight(w, n, k, ldw, q, ldq, scale);
+  if (st != kLaunch) return st;
   return hip_status(fp8rl::launch_quant_weight_block128(w, n, k, ldw, q, ldq, scale, as_stream(stream), pow2));
+}
+
+int fp8rl_quant_weight_block128_batched(const fp8rl_weight_job* jobs, int64_t count, void* stream) {
+  if (count < 0 || (count > 0 && !jobs)) return FP8RL_ERR_INVALID_ARG;
+  for (int64_t i = 0; i < count; ++i) {
+    const fp8rl_weight_job& j = jobs[i];
+    const int st = check_weight(j.w, j.n, j.k, j.ldw, j.q, j.ldq, j.scale);
+    if (st != kLaunch && st != FP8RL_OK) return st;
+  }
+  fp8rl::WeightJob chunk[fp8rl::kWeightBatchJobs];
+  for (int64_t i0 = 0; i0 < count; i0 += fp8rl::kWeightBatchJobs) {
+    const int c = (int)(count - i0 < fp8rl::kWeightBatchJobs ? count - i0 : fp8rl::kWeightBatchJobs);
+    for (int i = 0; i < c; ++i) {
+      const fp8rl_weight_job& j = jobs[i0 + i];
+      chunk[i] = fp8rl::WeightJob{j.w, j.n, j.k, j.ldw, j.q, j.ldq, j.scale};
+    }
+    const int st = hip_status(fp8rl::launch_quant_weight_block128_batched(chunk, c, as_stream(stream)));
+    if (st != FP8RL_OK) return st;
+  }
+  return FP8RL_OK;
 }
 
 int fp8rl_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k, int64_t ldw, uint8_t* q,

@@ -13,6 +13,19 @@ hipError_t launch_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k,
                                         uint8_t* q, int64_t ldq, float* scale, hipStream_t stream,
                                         bool pow2_scale);
 
+// Several weight matrices in one launch (at most kWeightBatchJobs, each already
+// validated like a single call; jobs with no blocks are skipped).  The total
+// block count must stay below 2^31.
+constexpr int kWeightBatchJobs = 64;
+struct WeightJob {
+  const uint16_t* w;
+  int64_t n, k, ldw;
+  uint8_t* q;
+  int64_t ldq;
+  float* scale;
+};
+hipError_t launch_quant_weight_block128_batched(const WeightJob* jobs, int count, hipStream_t stream);
+
 hipError_t launch_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
                                            uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
                                            hipStream_t stream, bool pow2_scale);

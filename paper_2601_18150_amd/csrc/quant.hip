@@ -98,11 +98,9 @@ __device__ __forceinline__ void store_stream8(uint8_t* p, const uint2& v) {
 // of a wave reads four 256-byte row segments.
 // ---------------------------------------------------------------------------
 template <bool kPow2Scale>
-__global__ __launch_bounds__(256) void quant_weight_block128_kernel(
-    const uint16_t* __restrict__ w, int64_t ldw, uint8_t* __restrict__ q, int64_t ldq,
-    float* __restrict__ scale, int nbk) {
-  __shared__ uint32_t red[4];
-  const int blk = blockIdx.x;
+__device__ __forceinline__ void quant_weight_block(const uint16_t* __restrict__ w, int64_t ldw,
+                                                   uint8_t* __restrict__ q, int64_t ldq,
+                                                   float* __restrict__ scale, int nbk, int blk, uint32_t* red) {
   const int bi = blk / nbk;
   const int bj = blk - bi * nbk;
   const int t = threadIdx.x;
@@ -136,6 +134,46 @@ __global__ __launch_bounds__(256) void quant_weight_block128_kernel(
 #pragma unroll
     for (int i = 0; i < 8; ++i) store_stream8(dst + (int64_t)(16 * i) * ldq, quant8<kMarkstein>(v[i], bs));
   }
+}
+
+template <bool kPow2Scale>
+__global__ __launch_bounds__(256) void quant_weight_block128_kernel(
+    const uint16_t* __restrict__ w, int64_t ldw, uint8_t* __restrict__ q, int64_t ldq,
+    float* __restrict__ scale, int nbk) {
+  __shared__ uint32_t red[4];
+  quant_weight_block<kPow2Scale>(w, ldw, q, ldq, scale, nbk, blockIdx.x, red);
+}
+
+// Many matrices in one launch: the job table travels in the kernel arguments
+// (constant memory, read with scalar loads); workgroup b quantises block
+// b - first_block of the last job whose first_block <= b.  One launch keeps the
+// memory pipeline full across matrices: a launch per matrix pays its ramp-up and
+// drain each time (about 2.5 us, measured on the 144-matrix resync pass).
+struct WeightJobArg {
+  const uint16_t* w;
+  uint8_t* q;
+  float* scale;
+  int64_t ldw, ldq;
+  int nbk;                 // k / 128
+  int first_block;         // blocks of the jobs before this one in the launch
+};
+
+struct WeightBatchArg {
+  WeightJobArg job[kWeightBatchJobs];
+  int count;
+};
+
+__global__ __launch_bounds__(256) void quant_weight_block128_batched_kernel(const WeightBatchArg b) {
+  __shared__ uint32_t red[4];
+  const int blk = blockIdx.x;
+  // binary search (wave-uniform) for the last job with first_block <= blk
+  int lo = 0, hi = b.count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (b.job[mid].first_block <= blk) lo = mid; else hi = mid - 1;
+  }
+  const WeightJobArg& j = b.job[lo];
+  quant_weight_block<false>(j.w, j.ldw, j.q, j.ldq, j.scale, j.nbk, blk - j.first_block, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -276,6 +314,28 @@ hipError_t launch_quant_weight_block128(const uint16_t* w, int64_t n, int64_t k,
   else
     hipLaunchKernelGGL(quant_weight_block128_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
                        w, ldw, q, ldq, scale, nbk);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_weight_block128_batched(const WeightJob* jobs, int count, hipStream_t stream) {
+  WeightBatchArg b;
+  b.count = 0;
+  int64_t blocks = 0;
+  for (int i = 0; i < count; ++i) {
+    const int64_t nb = (jobs[i].n / 128) * (jobs[i].k / 128);
+    if (nb == 0) continue;
+    WeightJobArg& j = b.job[b.count++];
+    j.w = jobs[i].w;
+    j.q = jobs[i].q;
+    j.scale = jobs[i].scale;
+    j.ldw = jobs[i].ldw;
+    j.ldq = jobs[i].ldq;
+    j.nbk = (int)(jobs[i].k / 128);
+    j.first_block = (int)blocks;
+    blocks += nb;
+  }
+  if (b.count == 0) return hipSuccess;
+  hipLaunchKernelGGL(quant_weight_block128_batched_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, b);
   return hipGetLastError();
 }
 

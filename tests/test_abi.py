@@ -71,6 +71,35 @@ def test_quant_weight_argument_errors(lib):
     assert f(None, 0, 0, 0, None, 0, None, None) == OK
 
 
+def test_quant_weight_batched_argument_errors(lib):
+    """Every job is validated before anything is launched: one bad job among good
+    ones returns its code (none of these calls reaches the GPU)."""
+    import paper_2601_18150_amd as fp8rl
+    f = lib.fp8rl_quant_weight_block128_batched
+
+    def jobs(*specs):
+        arr = (fp8rl.WeightJob * len(specs))()
+        for i, (w, n, k, ldw, q, ldq, sc) in enumerate(specs):
+            arr[i] = fp8rl.WeightJob(w, n, k, ldw, q, ldq, sc)
+        return ctypes.addressof(arr), arr
+
+    good = (A16, 128, 256, 256, A16, 256, A16)
+    assert f(None, -1, None) == INVALID
+    assert f(None, 3, None) == INVALID                                   # NULL array, count > 0
+    assert f(None, 0, None) == OK                                        # empty batch: no-op
+    for bad, code in [((A16, -128, 128, 128, A16, 128, A16), INVALID),
+                      ((A16, 128, 200, 200, A16, 208, A16), SHAPE),
+                      ((None, 128, 128, 128, A16, 128, A16), INVALID),
+                      ((A16, 128, 128, 120, A16, 128, A16), INVALID),     # ldw < k
+                      ((A4, 128, 128, 128, A16, 128, A16), MISALIGNED),
+                      ((A16, 128, 128, 128, A16, 136, A16), MISALIGNED)]:  # ldq % 16
+        for specs in ((bad,), (good, bad), (good, good, bad)):
+            p, keep = jobs(*specs)
+            assert f(p, len(specs), None) == code, (specs, code)
+    p, keep = jobs((A16, 0, 128, 128, A16, 128, A16), (None, 0, 0, 0, None, 0, None))
+    assert f(p, 2, None) == OK                                           # only empty jobs: no-op
+
+
 def test_quant_act_argument_errors(lib):
     f = lib.fp8rl_quant_act_token_group128
     assert f(A16, -1, 128, 128, A16, 128, A16, 1, None) == INVALID

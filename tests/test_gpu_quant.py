@@ -82,6 +82,65 @@ def test_quant_weight_exhaustive_element_map(fp8rl):
     assert_codes_equal(u8(q), qo, "codes")
 
 
+def test_quant_weight_batched_mixed_jobs(fp8rl):
+    """70 matrices (two launches of at most 64 jobs) of assorted shapes, padded
+    rows, empty jobs and special blocks: each equal to the oracle, padding untouched."""
+    announce("quant_weight batched: 70 mixed jobs")
+    rng = np.random.default_rng(5)
+    ws, qs, scs, pads, ref = [], [], [], [], []
+    for i in range(70):
+        n = 0 if i in (3, 40, 69) else 128 * int(rng.integers(1, 5))
+        k = 128 * int(rng.integers(1, 6))
+        pw, pq = (8 * int(rng.integers(0, 3)), 16 * int(rng.integers(0, 3))) if i % 3 == 0 else (0, 0)
+        w = synth.normal_bf16((max(n, 1), k), 0.02, 1000 + i, "cuda")[:n]
+        if n and i % 5 == 1:
+            synth.plant_special_blocks(w, 2000 + i, frac_zero=0.3, frac_large=0.3)
+        wbuf = torch.zeros((n, k + pw), dtype=torch.bfloat16, device="cuda")
+        wbuf[:, :k] = w
+        qbuf = torch.full((n, k + pq), 0xAB, dtype=torch.uint8, device="cuda")
+        ws.append(wbuf[:, :k])
+        qs.append(qbuf[:, :k])
+        scs.append(torch.full((n // 128, k // 128), -1.0, dtype=torch.float32, device="cuda"))
+        pads.append((qbuf, k))
+        ref.append(quant.quant_weight_block128(u16(w)) if n else None)
+    out = fp8rl.fp8rl_quant_weight_block128_batched(ws, qs, scs)
+    torch.cuda.synchronize()
+    for i, ((q, s), r, (qbuf, k)) in enumerate(zip(out, ref, pads)):
+        if r is None:
+            assert q.numel() == 0
+            continue
+        assert_codes_equal(u8(q), r[0], f"job {i} codes")
+        assert_scales_equal(f32(s), r[1], f"job {i} scales")
+        assert np.all(u8(qbuf[:, k:]) == 0xAB), f"job {i} wrote past k in a padded row"
+
+
+def test_quant_weight_batched_requant_layer(fp8rl):
+    """The four matrices of one resync layer in one call: equal to the C oracle."""
+    announce("quant_weight batched: resync layer 35")
+    mats = [synth.requant_matrix(35, name, device="cuda")[0] for name in synth.QWEN3_8B_LINEARS]
+    out = fp8rl.fp8rl_quant_weight_block128_batched(mats)
+    torch.cuda.synchronize()
+    for name, w, (q, s) in zip(synth.QWEN3_8B_LINEARS, mats, out):
+        qo, so = cref.quant_weight_block128(u16(w))
+        assert_codes_equal(u8(q), qo, f"{name} codes")
+        assert_scales_equal(f32(s), so, f"{name} scales")
+
+
+def test_quant_weight_batched_exhaustive_element_map(fp8rl):
+    """The exhaustive (x, amax) sweep through the batched kernel, split into three
+    jobs of unequal row ranges."""
+    announce("quant_weight batched exhaustive sweep")
+    w = synth.sweep_weight_blocks("cuda")
+    nb = w.shape[0] // 128
+    cuts = [0, 128 * (nb // 3), 128 * (nb // 3 + nb // 5), w.shape[0]]
+    parts = [w[a:b] for a, b in zip(cuts, cuts[1:])]
+    out = fp8rl.fp8rl_quant_weight_block128_batched(parts)
+    torch.cuda.synchronize()
+    qo, so = cref.quant_weight_block128(u16(w))
+    assert_scales_equal(np.concatenate([f32(s) for _, s in out]), so, "scales")
+    assert_codes_equal(np.concatenate([u8(q) for q, _ in out]), qo, "codes")
+
+
 def test_quant_act_tiny(fp8rl):
     announce("quant_act tiny 64x512")
     a, _ = synth.tiny_linear(device="cuda")
