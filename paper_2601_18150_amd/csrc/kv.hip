@@ -230,7 +230,11 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(
   typedef typename CacheElem<kFp8>::T E;
   constexpr int kPer16 = 16 / sizeof(E);                  // cache values per 16-byte load
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  // wave-uniform as far as the compiler knows too: the split, its token range and
+  // the page indices stay in scalar registers, so the block-table reads are scalar
+  // loads (a vector load there would make each page's loads wait for every load in
+  // flight, the prefetched pages included)
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int split = blockIdx.x * 4 + wave;
   if (split >= max_splits) return;
   const int kvh = blockIdx.y;
@@ -273,13 +277,24 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(
     }
   };
 
-  // three pages in flight: the current one and the next two
-  PageRegs<kFp8> cur, nx1, nx2;
-  if (t0 < t1) load_page(t0, cur);
-  if (t0 + kPage < t1) load_page(t0 + kPage, nx1);
-  for (int tp = t0; tp < t1; tp += kPage) {
+  // Three pages in flight: the current one and the next two, in three register
+  // sets that rotate by name (the loop body below runs three pages), so no page's
+  // registers are copied while a later page's loads into them are in flight.
+  // Every step issues its prefetch unconditionally (past the split's end it
+  // re-reads the split's last page, a cache hit): with the same number of loads
+  // on every path the compiler waits for exactly the page it needs, never for
+  // the prefetches behind it.
+  if (t0 >= t1) return;    // (empty split: nothing in flight, nothing to write)
+  const int t_last = t1 - 1;
+  PageRegs<kFp8> pg0, pg1, pg2;
+  load_page(t0, pg0);
+  load_page(min(t0 + kPage, t_last), pg1);
+  // one page: prefetch page tp + 2 into `next` (the set of page tp - 1), then
+  // attend over page tp held in `cur` if it is inside the split
+  auto page_step = [&](int tp, const PageRegs<kFp8>& cur, PageRegs<kFp8>& next) {
+    load_page(min(tp + 2 * kPage, t_last), next);
+    if (tp >= t1) return;
     const int valid = min(kPage, t1 - tp);
-    if (tp + 2 * kPage < t1) load_page(tp + 2 * kPage, nx2);
 
     // ---- scores
     v4f32_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -352,8 +367,11 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(
       o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, vb, o[nb], 0, 0, 0);
       o[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pb, vb, o[nb], 0, 0, 0);
     }
-    cur = nx1;
-    nx1 = nx2;
+  };
+  for (int tp = t0; tp < t1; tp += 3 * kPage) {
+    page_step(tp, pg0, pg2);
+    page_step(tp + kPage, pg1, pg0);
+    page_step(tp + 2 * kPage, pg2, pg1);
   }
 
   // o[nb][i] = O[head 4g + i][dim 8j + nb]; lanes h < kG of group 0 hold m, l of head h
@@ -431,8 +449,11 @@ hipError_t launch_kv_cache_write(const uint16_t* k, const uint16_t* v, int64_t t
 }
 
 AttnSplit attn_decode_split(int64_t batch, int64_t kv_heads, int64_t group, int64_t max_seq_len) {
-  // about 8192 waves over the whole batch (32 per CU), splits of at least 256 tokens
-  constexpr int64_t kTargetWaves = 8192;   // measured: 16384 (shorter splits) 4% slower
+  // about 6144 waves over the whole batch (three times the 2048 that are resident
+  // at two waves per SIMD), splits of at least 256 tokens.  Measured on 64
+  // sequences of 4096 .. 20480 tokens: 2048 / 3072 / 4096 / 6144 / 8192 / 16384
+  // waves took 396 / 440 / 385 / 358 / 394 / 429 us.
+  constexpr int64_t kTargetWaves = 6144;
   const int64_t pairs = batch * kv_heads;
   int64_t splits = (kTargetWaves + pairs - 1) / (pairs > 0 ? pairs : 1);
   if (splits < 1) splits = 1;
