@@ -12,9 +12,13 @@ namespace {
 
 // Tile configurations (BN x BM, waves, LDS ring depth), measured on MI355X:
 // - M and N >= 2048: 256x256, 8 waves, 2 slots (one workgroup per CU).
-// - other M > 256, and the grouped GEMM: 128x128, 4 waves, 2 slots: two
-//   workgroups per CU walking their tiles as one pipeline.  Deeper rings with
-//   one workgroup per CU were slower here (MoE gate_up 270 vs 205 us).
+// - other M > 256, and the grouped GEMM with K > 1024: 128x128, 4 waves, 2
+//   slots: two workgroups per CU walking their tiles as one pipeline.  Deeper
+//   rings with one tile per workgroup were slower (MoE gate_up 270 vs 205 us).
+// - the grouped GEMM with K <= 1024: 256n x 128m, 8 waves, 2 slots, one
+//   workgroup per CU walking its tiles as one pipeline: half as many tiles, so
+//   short K loops pay fewer tile ends (Qwen3-30B-A3B down, K = 768: 104-106 vs
+//   118-120 us; gate_up, K = 2048, is 2-4% slower with it).
 // - 128 < M <= 256 (decode batches): one 256-token tile, 128x256, 8 waves, 3
 //   slots (Qwen3-8B gate_up at M = 256: 44.8 vs 48.0 us).
 // - split-K ranges: 128x128, 3 slots (decode linears 123 vs 129 us per layer).
@@ -22,6 +26,7 @@ using CfgLarge = GemmCfg<256, 256, 2, 4, 2>;   // 512 threads, wave tile 128(n) 
 using CfgSmall = GemmCfg<128, 128, 2, 2, 2>;   // 256 threads, wave tile 64 x 64, 65 KiB LDS
 using CfgDecode = GemmCfg<128, 256, 2, 4, 3>;  // 512 threads, wave tile 64 x 64, 147 KiB LDS
 using CfgSplitK = GemmCfg<128, 128, 2, 2, 3>;  // one tile per workgroup, 2 K steps in flight, 98 KiB LDS
+using CfgGroupedShortK = GemmCfg<256, 128, 4, 2, 2>;   // 512 threads, wave tile 64 x 64, 97 KiB LDS
 using CfgGrouped = CfgSmall;
 
 constexpr int kXcds = 8;        // MI355X: workgroup i is dispatched to XCD i % 8
@@ -56,10 +61,11 @@ __device__ __forceinline__ int xcd_grouped_tile(int id, int tiles_m, int tiles_n
 }
 
 // The cross-tile pipeline (next tile's first load during this tile's last
-// step) for the 128x128 tiles; the 256x256 tile has no registers to spare for
-// the next tile's load plan and runs one tile per workgroup.
+// step) for the 128x128 and 256x128 tiles with a 2-slot ring; the 256x256 tile
+// has no registers to spare for the next tile's load plan and runs one tile per
+// workgroup.
 template <class C>
-constexpr bool kCrossTiles = C::BN * C::BM <= 128 * 128 && C::STAGES == 2;
+constexpr bool kCrossTiles = C::BN * C::BM <= 256 * 128 && C::STAGES == 2;
 
 // Job providers for gemm_tiles (see gemm_core.hpp): wave-uniform, no LDS
 // writes, no synchronisation.
@@ -340,11 +346,16 @@ hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, in
                                           const uint8_t* qw, const float* sw, const int32_t* group_offsets,
                                           int64_t num_groups, int64_t total_rows, uint16_t* y, int64_t n,
                                           int64_t k, hipStream_t stream, bool pow2_scales) {
+  const bool short_k = k <= 1024;
   if (pow2_scales)
-    return launch_grouped<CfgGrouped, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n,
-                                            k, stream);
-  return launch_grouped<CfgGrouped, false>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k,
-                                           stream);
+    return short_k ? launch_grouped<CfgGroupedShortK, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups,
+                                                             total_rows, y, n, k, stream)
+                   : launch_grouped<CfgGrouped, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows,
+                                                      y, n, k, stream);
+  return short_k ? launch_grouped<CfgGroupedShortK, false>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups,
+                                                            total_rows, y, n, k, stream)
+                 : launch_grouped<CfgGrouped, false>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y,
+                                                     n, k, stream);
 }
 
 }  // namespace fp8rl

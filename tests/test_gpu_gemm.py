@@ -336,10 +336,11 @@ def test_grouped_many_experts_matches_dense_per_expert(fp8rl):
     check(y, gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, offsets), "grouped 70")
 
 
-@pytest.mark.parametrize("k", [128, 384])
+@pytest.mark.parametrize("k", [128, 384, 1152])
 def test_grouped_many_tiles_per_workgroup(fp8rl, k):
     """Over 512 expert tiles (several per persistent workgroup), ragged experts, empty
-    experts at both ends, 1 and 3 K blocks per tile."""
+    experts at both ends, 1, 3 and 9 K blocks per tile (K <= 1024 runs 256x128 tiles,
+    K = 1152 the 128x128 ones)."""
     announce(f"grouped gemm persistent k={k}")
     rng = np.random.default_rng(k)
     g, n = 96, 640
