@@ -19,12 +19,16 @@ namespace {
 //   workgroup per CU walking its tiles as one pipeline: half as many tiles, so
 //   short K loops pay fewer tile ends (Qwen3-30B-A3B down, K = 768: 104-106 vs
 //   118-120 us; gate_up, K = 2048, is 2-4% slower with it).
-// - 128 < M <= 256 (decode batches): one 256-token tile, 128x256, 8 waves, 3
-//   slots (Qwen3-8B gate_up at M = 256: 44.8 vs 48.0 us).
+// - 128 < M <= 256 (decode batches): 64x64 tiles, 4 waves, 3 slots, one tile per
+//   workgroup, when they number at most 512 (Qwen3-8B at M = 256: qkv 21.6 vs
+//   24.0 us, o_proj 17.0 vs 21.3 us for split-K 128x128 tiles); otherwise one
+//   256-token tile, 128x256, 8 waves, 3 slots (gate_up: 44 vs 48 us for 128x128,
+//   59 us for 64x64).
 // - split-K ranges: 128x128, 3 slots (decode linears 123 vs 129 us per layer).
 using CfgLarge = GemmCfg<256, 256, 2, 4, 2>;   // 512 threads, wave tile 128(n) x 64(m), 130 KiB LDS
 using CfgSmall = GemmCfg<128, 128, 2, 2, 2>;   // 256 threads, wave tile 64 x 64, 65 KiB LDS
 using CfgDecode = GemmCfg<128, 256, 2, 4, 3>;  // 512 threads, wave tile 64 x 64, 147 KiB LDS
+using CfgDecodeNarrow = GemmCfg<64, 64, 2, 2, 3>;   // 256 threads, wave tile 32 x 32, 49 KiB LDS
 using CfgSplitK = GemmCfg<128, 128, 2, 2, 3>;  // one tile per workgroup, 2 K steps in flight, 98 KiB LDS
 using CfgGroupedShortK = GemmCfg<256, 128, 4, 2, 2>;   // 512 threads, wave tile 64 x 64, 97 KiB LDS
 using CfgGrouped = CfgSmall;
@@ -293,16 +297,22 @@ hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, con
 
 }  // namespace
 
+// Decode batches (128 < M <= 256) whose 64x64 tiles number at most 512 (two per CU).
+static bool decode_narrow_tiles(int64_t m, int64_t n) { return ((m + 63) / 64) * (n / 64) <= 512; }
+
 hipError_t launch_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
                                   const uint8_t* qw, int64_t ldw, const float* sw, uint16_t* y, int64_t ldy,
                                   int64_t m, int64_t n, int64_t k, hipStream_t stream, bool pow2_scales) {
   const bool large = m >= 2048 && n >= 2048;
   const bool decode = !large && m > 128 && m <= 256;
+  const bool narrow = decode && decode_narrow_tiles(m, n);
   if (pow2_scales)
     return large    ? launch_dense<CfgLarge, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+           : narrow ? launch_dense<CfgDecodeNarrow, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
            : decode ? launch_dense<CfgDecode, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
                     : launch_dense<CfgSmall, true>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
   return large    ? launch_dense<CfgLarge, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
+         : narrow ? launch_dense<CfgDecodeNarrow, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
          : decode ? launch_dense<CfgDecode, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream)
                   : launch_dense<CfgSmall, false>(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, stream);
 }
@@ -315,6 +325,9 @@ int splitk_factor(int64_t m, int64_t n, int64_t k) {
   // grows with the split.)
   constexpr int64_t kCus = 256;
   if (m <= 0 || n <= 0 || k <= 0 || (m >= 2048 && n >= 2048)) return 1;
+  // decode batches run unsplit on 64x64 tiles when K is short enough for one
+  // workgroup's K loop (Qwen3-8B qkv, o_proj: K = 4096; down, K = 12288, splits)
+  if (m > 128 && m <= 256 && k <= 4096 && decode_narrow_tiles(m, n)) return 1;
   const int64_t tiles = ((m + 127) / 128) * (n / 128);
   if (2 * tiles >= kCus) return 1;
   int64_t s = 1;

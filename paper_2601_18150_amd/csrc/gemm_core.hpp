@@ -411,7 +411,7 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       // layout wrote partial cache lines (1.6x the output bytes reached HBM)
       // and let the output displace the operands in the memory-side cache.
       // Staging layout: rows of BN bf16; 16-byte chunk c of row r (counted
-      // within the row group) sits at c ^ (r & 15), so the 16 rows of one
+      // within the row group) sits at c ^ (r & 15) (r & 7 for 64-wide tiles), so the 16 rows of one
       // fragment store, and the rows of one read-back wave instruction, spread
       // evenly over the 64 banks.  Row groups of kRows rows fit one slot (or,
       // without kCross, the whole ring).
@@ -420,7 +420,9 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       constexpr int kSpace = kCross ? C::kStageBytes : C::kLdsBytes;
       constexpr int kRowsFit = kSpace / kRowBytes;
       constexpr int kRows = kRowsFit >= C::BM ? C::BM : (kRowsFit / C::WTM) * C::WTM;
-      static_assert(kChunks >= 16 && kRows >= C::WTM && C::BM % kRows == 0, "bf16 staging must fit");
+      static_assert(kChunks % 8 == 0 && kRows >= C::WTM && C::BM % kRows == 0, "bf16 staging must fit");
+      // (64-wide tiles: 8 chunks per row, key r & 7, which keeps the XOR inside the row)
+      constexpr int kSwz = kChunks % 16 == 0 ? 15 : 7;
       uint8_t* stage = kCross ? lds + (slot ^ 1) * C::kStageBytes : lds;
 #pragma unroll
       for (int g0 = 0; g0 < C::BM; g0 += kRows) {
@@ -435,7 +437,7 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
               uint2 o;
               o.x = f32_to_bf16_rne(acc[tn][tm][0]) | (f32_to_bf16_rne(acc[tn][tm][1]) << 16);
               o.y = f32_to_bf16_rne(acc[tn][tm][2]) | (f32_to_bf16_rne(acc[tn][tm][3]) << 16);
-              *reinterpret_cast<uint2*>(stage + ml * kRowBytes + (((nl >> 3) ^ (ml & 15)) << 4) + ((nl >> 2) & 1) * 8) = o;
+              *reinterpret_cast<uint2*>(stage + ml * kRowBytes + (((nl >> 3) ^ (ml & kSwz)) << 4) + ((nl >> 2) & 1) * 8) = o;
             }
           }
         }
@@ -444,7 +446,7 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
 #pragma unroll 4
         for (int r = t / kChunks; r < kRows; r += C::kThreads / kChunks) {
           if (g0 + r < cur.m_valid && c * 8 < n_valid) {
-            const uint4 v = *reinterpret_cast<const uint4*>(stage + r * kRowBytes + ((c ^ (r & 15)) << 4));
+            const uint4 v = *reinterpret_cast<const uint4*>(stage + r * kRowBytes + ((c ^ (r & kSwz)) << 4));
             store_stream16(y + (int64_t)(cur.row_lo + g0 + r) * ldy + cur.n0 + c * 8, v);
           }
         }

@@ -119,7 +119,7 @@ def run_dense_ue8m0(fp8rl, qa, sa, qw, sw, ldsa_pad=0):
     return y
 
 
-@pytest.mark.parametrize("m,n,k", [(1, 128, 128), (37, 384, 256), (129, 640, 384), (256, 1152, 1280), (300, 512, 256),
+@pytest.mark.parametrize("m,n,k", [(1, 128, 128), (37, 384, 256), (129, 640, 384), (256, 1152, 1280), (200, 16512, 256), (300, 512, 256),
                                    (2048, 2048, 256), (2100, 2176, 384), (1000, 16384, 128)])
 def test_gemm_ue8m0_shapes(fp8rl, m, n, k):
     announce(f"gemm_ue8m0 m={m} n={n} k={k}")
