@@ -134,9 +134,11 @@ def test_gemm_workspace_size(lib):
     """The split-K workspace is a pure function of the shape: splits x M x N fp32."""
     f = lib.fp8rl_gemm_w8a8_block_workspace_size
     assert f(256, 4096, 12288) == 4 * 256 * 4096 * 4      # decode down: 64 tiles -> 4 splits of 24 K blocks
-    assert f(256, 6144, 4096) == 2 * 256 * 6144 * 4       # decode qkv: 96 tiles -> 2 splits
-    assert f(256, 4096, 4096) == 4 * 256 * 4096 * 4       # decode o_proj: 4 splits of 8 K blocks
-    assert f(256, 24576, 4096) == 0                       # 384 tiles fill the GPU
+    assert f(256, 6144, 4096) == 0                        # decode qkv: 384 unsplit 64x64 tiles
+    assert f(256, 4096, 4096) == 0                        # decode o_proj: 256 unsplit 64x64 tiles
+    assert f(256, 24576, 4096) == 0                       # 384 tiles of 128x128 fill the GPU
+    assert f(128, 4096, 4096) == 8 * 128 * 4096 * 4       # M <= 128: 32 tiles of 128x128 -> 8 splits of 4 K blocks
+    assert f(300, 6144, 4096) == 0                        # M > 256: 144 tiles of 128x128, over half the CUs
     assert f(8192, 24576, 4096) == 0                      # 256x256 tiles, never split
     assert f(64, 512, 512) == 0                           # 4 K blocks: no split shorter than 4
     assert f(37, 384, 13 * 128) == 3 * 37 * 384 * 4       # uneven split of 13 K blocks
