@@ -129,6 +129,26 @@ def test_gemm_many_tiles_per_workgroup(fp8rl, m, n, k):
     check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"{m}x{n}x{k}")
 
 
+@pytest.mark.parametrize("m,n,k", [(2048, 2048, 256), (300, 384, 384), (256, 256, 256)])
+def test_gemm_largest_row_pitch(fp8rl, m, n, k):
+    """Operand row pitches of 2^24 - 16 bytes, the largest the entry point accepts: the
+    DMA's 32-bit in-tile offsets reach 255 rows x pitch (256x256 tiles, 4.28e9 of the 2^32
+    range), 127 rows (128x128 tiles) and 63 rows (64x64 decode tiles).  Only the first k
+    bytes of each row are written; the buffers are 2048 x 16 MiB for the first case."""
+    announce(f"gemm largest row pitch m={m} n={n} k={k}")
+    pitch = (1 << 24) - 16
+    qa, sa, qw, sw = quantised_operands(m, n, k, m + n + 5 * k)
+    a_big = torch.empty((m, pitch), dtype=torch.uint8, device="cuda")
+    w_big = torch.empty((n, pitch), dtype=torch.uint8, device="cuda")
+    a_big[:, :k] = to_dev(qa)
+    w_big[:, :k] = to_dev(qw)
+    y = fp8rl.fp8rl_gemm_w8a8_block(a_big[:, :k], to_dev(sa), w_big[:, :k], to_dev(sw))
+    torch.cuda.synchronize()
+    del a_big, w_big
+    torch.cuda.empty_cache()
+    check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"pitch {pitch} {m}x{n}x{k}")
+
+
 def test_gemm_full_range_codes_within_accumulation_bound(fp8rl):
     """Uniformly random codes over the whole E4M3 range (products up to 448^2 with
     heavy cancellation inside a K block).
