@@ -701,7 +701,7 @@ def cpu_baseline(a, w, chunk=1024, min_seconds=10.0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; multi-GPU runs are not part of it",
+        print(json.dumps({"error": "bench.py runs on one GPU; runs on several GPUs are not supported",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import paper_2601_18150_amd as fp8rl
