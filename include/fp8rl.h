@@ -198,6 +198,34 @@ int fp8rl_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld
                                   void* stream);
 
 /*
+ * The grouped GEMM over gathered rows: MoE dispatch and expert product in one
+ * pass.  Per-token quantisation commutes with copying rows (section 2.1.1:
+ * one scale per token and 128-wide group), so tokens are quantised once and
+ * each expert reads its tokens' codes and scales directly:
+ *   y[r] = (grouped product above)[r] with activation row row_index[r],
+ * i.e. exactly fp8rl_gather_rows_fp8(row_index) followed by
+ * fp8rl_grouped_gemm_w8a8_block, without the gathered copy (bit-identical
+ * results: the same sums in the same order).
+ *
+ * qa         [src_rows][lda] E4M3 codes of the tokens; lda >= k, lda % 16 == 0
+ * sa         [k/128][ld_sa] fp32 token scales; ld_sa >= src_rows
+ * src_rows   >= 1 when total_rows > 0; src_rows * lda < 2^32 (else
+ *            FP8RL_ERR_UNSUPPORTED_SHAPE)
+ * row_index  DEVICE int32 [total_rows]: the token of each expert-ordered row
+ *            (precondition 0 <= row_index[r] < src_rows; an index outside is
+ *            clamped into range, reading a wrong row, never out of bounds)
+ * qw, sw, group_offsets, num_groups, total_rows, y, n, k: as above.
+ * Alignment: qa, qw, y 16-byte aligned; sa, sw, group_offsets, row_index
+ * 4-byte aligned.
+ */
+int fp8rl_grouped_gemm_w8a8_block_gathered(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                           int64_t src_rows, const int32_t* row_index,
+                                           const uint8_t* qw, const float* sw,
+                                           const int32_t* group_offsets, int64_t num_groups,
+                                           int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
+                                           void* stream);
+
+/*
  * Power-of-two (UE8M0) scale variant (section 2.4.3, "Scaling Factor: FP32 vs
  * Power-of-2": the same 128x128 / 1x128 blocks with scales restricted to 2^k).
  * Same arguments, layouts, error codes and alignment rules as the fp32-scale

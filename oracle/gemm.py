@@ -63,6 +63,26 @@ def grouped_gemm_ref_fp64(qa, sa, qw, sw, offsets) -> np.ndarray:
     return y
 
 
+def grouped_gemm_gathered_ref_fp64(qa_src, sa_src, row_index, qw, sw, offsets) -> np.ndarray:
+    """The grouped product over gathered rows: row r (expert-grouped order) uses
+    activation row row_index[r] of qa_src [T][K] and its scales sa_src[:, row_index[r]].
+    Per-token scales make quantising commute with copying rows, so this is the
+    dispatch of already-quantised tokens followed by the per-expert product.
+    """
+    row_index = np.asarray(row_index, dtype=np.int64)
+    offsets = np.asarray(offsets, dtype=np.int64)
+    g, n, k = qw.shape
+    y = np.zeros((row_index.size, n), dtype=np.float64)
+    for e in range(g):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        if hi <= lo:
+            continue
+        rows = row_index[lo:hi]
+        a = dequant_act(np.asarray(qa_src)[rows], np.asarray(sa_src)[:, rows])
+        y[lo:hi] = a @ dequant_weight(qw[e], sw[e]).T
+    return y
+
+
 def gemm_blockwise_bruteforce(qa, sa, qw, sw) -> np.ndarray:
     """The same product written as the blockwise sum, with explicit Python loops.
 

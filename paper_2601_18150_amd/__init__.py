@@ -22,7 +22,7 @@ import torch  # loads torch's HIP runtime first, so libfp8rl binds to that same 
 __all__ = [
     "LIB_PATH", "Fp8rlError", "load",
     "fp8rl_quant_weight_block128", "fp8rl_quant_weight_block128_batched", "fp8rl_quant_act_token_group128",
-    "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block",
+    "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block_gathered",
     "fp8rl_gemm_w8a8_block_workspace_size", "fp8rl_gemm_w8a8_block_ws",
     "fp8rl_quant_weight_block128_ue8m0", "fp8rl_quant_act_token_group128_ue8m0",
     "fp8rl_gemm_w8a8_block_ue8m0", "fp8rl_grouped_gemm_w8a8_block_ue8m0",
@@ -67,6 +67,7 @@ def _load():
         "fp8rl_quant_act_token_group128": [P, I, I, I, P, I, P, I, P],
         "fp8rl_gemm_w8a8_block": [P, I, P, I, P, I, P, P, I, I, I, I, P],
         "fp8rl_grouped_gemm_w8a8_block": [P, P, I, P, P, P, I, I, P, I, I, P],
+        "fp8rl_grouped_gemm_w8a8_block_gathered": [P, I, P, I, I, P, P, P, P, I, I, P, I, I, P],
         "fp8rl_gemm_w8a8_block_ws": [P, I, P, I, P, I, P, P, I, I, I, I, P, I, P],
         "fp8rl_quant_weight_block128_ue8m0": [P, I, I, I, P, I, P, P],
         "fp8rl_quant_act_token_group128_ue8m0": [P, I, I, I, P, I, P, I, P],
@@ -375,6 +376,44 @@ def _grouped(name, qa, sa, qw, sw, group_offsets, y, stream):
         return y
     st = getattr(load(), name)(qa.data_ptr(), sa.data_ptr(), sa.stride(0), qw.data_ptr(), sw.data_ptr(),
                                group_offsets.data_ptr(), g, r, y.data_ptr(), n, k, _stream(stream))
+    _check(name, st)
+    return y
+
+
+def fp8rl_grouped_gemm_w8a8_block_gathered(qa: torch.Tensor, sa: torch.Tensor, row_index: torch.Tensor,
+                                           qw: torch.Tensor, sw: torch.Tensor, group_offsets: torch.Tensor,
+                                           y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The grouped product over gathered rows: row r of y (expert-grouped order) uses
+    token row_index[r] of qa [T][K] (row pitch allowed) and sa [K/128][ld >= T];
+    equal bit for bit to fp8rl_gather_rows_fp8 followed by fp8rl_grouped_gemm_w8a8_block."""
+    name = "fp8rl_grouped_gemm_w8a8_block_gathered"
+    qa, qw = _u8(qa), _u8(qw)
+    t, k = qa.shape
+    g, n, k2 = qw.shape
+    if k != k2:
+        raise ValueError("K mismatch")
+    if not qw.is_contiguous() or not sw.is_contiguous():
+        raise ValueError("qw and sw must be contiguous")
+    if sw.numel() != g * (n // 128) * (k // 128) or sw.dtype != torch.float32:
+        raise ValueError("sw must be fp32 [G][N/128][K/128]")
+    if sa.dtype != torch.float32 or sa.dim() != 2 or sa.size(0) != k // 128 or sa.stride(1) != 1 or sa.size(1) < t:
+        raise ValueError("sa must be fp32 [K/128][ld >= T]")
+    if row_index.dtype != torch.int32 or row_index.dim() != 1 or not row_index.is_contiguous():
+        raise ValueError("row_index must be a contiguous 1-D int32 tensor")
+    if group_offsets.dtype != torch.int32 or group_offsets.numel() != g + 1 or not group_offsets.is_contiguous():
+        raise ValueError("group_offsets must be a contiguous int32 tensor of G+1 entries")
+    r = row_index.numel()
+    if y is None:
+        y = torch.empty((r, n), dtype=torch.bfloat16, device=qa.device)
+    if y.dtype != torch.bfloat16 or tuple(y.shape) != (r, n) or not y.is_contiguous():
+        raise ValueError("y must be contiguous bf16 [R][N]")
+    _dev(qa, sa, row_index, qw, sw, group_offsets, y)
+    if r == 0:
+        return y
+    st = load().fp8rl_grouped_gemm_w8a8_block_gathered(qa.data_ptr(), _ld(qa), sa.data_ptr(), sa.stride(0), t,
+                                                       row_index.data_ptr(), qw.data_ptr(), sw.data_ptr(),
+                                                       group_offsets.data_ptr(), g, r, y.data_ptr(), n, k,
+                                                       _stream(stream))
     _check(name, st)
     return y
 

@@ -221,6 +221,29 @@ int fp8rl_grouped_gemm_w8a8_block_ue8m0(const uint8_t* qa, const float* sa, int6
   return grouped(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y, n, k, stream, true);
 }
 
+int fp8rl_grouped_gemm_w8a8_block_gathered(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                           int64_t src_rows, const int32_t* row_index, const uint8_t* qw,
+                                           const float* sw, const int32_t* group_offsets, int64_t num_groups,
+                                           int64_t total_rows, uint16_t* y, int64_t n, int64_t k, void* stream) {
+  if (total_rows < 0 || n < 0 || k < 0 || src_rows < 0) return FP8RL_ERR_INVALID_ARG;
+  if (num_groups < 1) return FP8RL_ERR_INVALID_ARG;
+  if (n % 128 || k % 128) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (total_rows >= kMaxDim || n >= kMaxDim || k >= kMaxLd || num_groups > 1024 || src_rows >= kMaxDim ||
+      (total_rows / 128 + num_groups) * (n / 128) >= (int64_t(1) << 31))
+    return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (total_rows == 0 || n == 0) return FP8RL_OK;
+  if (!qa || !sa || !qw || !sw || !group_offsets || !y || !row_index || src_rows == 0) return FP8RL_ERR_INVALID_ARG;
+  if (k == 0) return FP8RL_ERR_UNSUPPORTED_SHAPE;
+  if (lda < k || ld_sa < src_rows) return FP8RL_ERR_INVALID_ARG;
+  if (src_rows * lda >= (int64_t(1) << 32)) return FP8RL_ERR_UNSUPPORTED_SHAPE;   // 32-bit DMA offsets
+  if (!aligned(qa, 16) || !aligned(qw, 16) || !aligned(y, 16) || !aligned(sa, 4) || !aligned(sw, 4) ||
+      !aligned(group_offsets, 4) || !aligned(row_index, 4) || lda % 16)
+    return FP8RL_ERR_MISALIGNED;
+  return hip_status(fp8rl::launch_grouped_gemm_w8a8_block_gathered(qa, lda, sa, ld_sa, src_rows, row_index, qw, sw,
+                                                                   group_offsets, num_groups, total_rows, y, n, k,
+                                                                   as_stream(stream)));
+}
+
 static int grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw, const float* sw,
                    const int32_t* group_offsets, int64_t num_groups, int64_t total_rows, uint16_t* y, int64_t n,
                    int64_t k, void* stream, bool pow2) {

@@ -219,11 +219,14 @@ struct GroupedJobs {
   }
 };
 
-template <class C, bool kMx>
+// kGather: output row r takes its activation row from source row gidx[r] of qa
+// ([src_rows][lda]) and sa ([K/128][ld_sa]); otherwise qa is [rows][K].
+template <class C, bool kMx, bool kGather>
 __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
     const uint8_t* __restrict__ qa, const float* __restrict__ sa, int64_t ld_sa,
     const uint8_t* __restrict__ qw, const float* __restrict__ sw,
-    const int32_t* __restrict__ offsets, int G, uint16_t* __restrict__ y, int64_t N, int64_t K, int tiles_n) {
+    const int32_t* __restrict__ offsets, int G, uint16_t* __restrict__ y, int64_t N, int64_t K, int tiles_n,
+    const int32_t* __restrict__ gidx, int src_rows, int64_t lda) {
   // one LDS object: the ring, then the two expert tables
   __shared__ __attribute__((aligned(16))) uint8_t lds[C::kLdsBytes + 2 * 4 * (kMaxExperts + 1)];
   int* tstart = reinterpret_cast<int*>(lds + C::kLdsBytes);
@@ -254,8 +257,9 @@ __global__ __launch_bounds__(C::kThreads) void grouped_gemm_w8a8_block_kernel(
   GroupedJobs<C> jobs{(int)blockIdx.x, (int)gridDim.x, __builtin_amdgcn_readfirstlane(tstart[G]), tiles_n, G,
                       tstart, rstart, N, K};
   const int KB = (int)(K / 128);
-  gemm_tiles<C, false, kCrossTiles<C>, GroupedJobs<C>, kMx>(qa, K, sa, ld_sa, qw, K, sw, KB, y, N, nullptr, (int)N,
-                                                            KB, jobs, lds);
+  gemm_tiles<C, false, kCrossTiles<C>, GroupedJobs<C>, kMx, kGather>(qa, kGather ? lda : K, sa, ld_sa, qw, K, sw, KB,
+                                                                     y, N, nullptr, (int)N, KB, jobs, lds, gidx,
+                                                                     src_rows);
 }
 
 // Workgroups that stay resident on one CU for a configuration (LDS-limited).
@@ -280,18 +284,19 @@ hipError_t launch_dense(const uint8_t* qa, int64_t lda, const float* sa, int64_t
   return hipGetLastError();
 }
 
-template <class C, bool kMx>
+template <class C, bool kMx, bool kGather = false>
 hipError_t launch_grouped(const uint8_t* qa, const float* sa, int64_t ld_sa, const uint8_t* qw,
                           const float* sw, const int32_t* offsets, int64_t g, int64_t rows, uint16_t* y,
-                          int64_t n, int64_t k, hipStream_t stream) {
+                          int64_t n, int64_t k, hipStream_t stream, const int32_t* gidx = nullptr,
+                          int64_t src_rows = 0, int64_t lda = 0) {
   const int64_t max_tiles_m = rows / C::BM + g;        // upper bound on the real m tiles
   const int64_t tiles_n = (n + C::BN - 1) / C::BN;
   const int64_t total = max_tiles_m * tiles_n;
   // persistent grid with the cross-tile pipeline, else one workgroup per tile
   const int64_t slots = kCrossTiles<C> ? (int64_t)kCus * per_cu<C, 2 * 4 * (kMaxExperts + 1)>() : total;
-  hipLaunchKernelGGL((grouped_gemm_w8a8_block_kernel<C, kMx>), dim3((unsigned)(total < slots ? total : slots)),
-                     dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw, sw, offsets, (int)g, y, n, k,
-                     (int)tiles_n);
+  hipLaunchKernelGGL((grouped_gemm_w8a8_block_kernel<C, kMx, kGather>),
+                     dim3((unsigned)(total < slots ? total : slots)), dim3(C::kThreads), 0, stream, qa, sa, ld_sa, qw,
+                     sw, offsets, (int)g, y, n, k, (int)tiles_n, gidx, (int)src_rows, lda);
   return hipGetLastError();
 }
 
@@ -369,6 +374,18 @@ hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, in
                                                             total_rows, y, n, k, stream)
                  : launch_grouped<CfgGrouped, false>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y,
                                                      n, k, stream);
+}
+
+hipError_t launch_grouped_gemm_w8a8_block_gathered(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                                   int64_t src_rows, const int32_t* row_index, const uint8_t* qw,
+                                                   const float* sw, const int32_t* group_offsets, int64_t num_groups,
+                                                   int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
+                                                   hipStream_t stream) {
+  if (k <= 1024)
+    return launch_grouped<CfgGroupedShortK, false, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups,
+                                                         total_rows, y, n, k, stream, row_index, src_rows, lda);
+  return launch_grouped<CfgGrouped, false, true>(qa, sa, ld_sa, qw, sw, group_offsets, num_groups, total_rows, y,
+                                                 n, k, stream, row_index, src_rows, lda);
 }
 
 }  // namespace fp8rl

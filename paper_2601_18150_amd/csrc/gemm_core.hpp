@@ -207,15 +207,24 @@ struct TileJob {
 // the only vector-memory traffic of the loop, so the one explicit vmcnt wait
 // per step is the only wait on global memory (at a tile's first step it also
 // covers the previous tile's output stores).
-template <class C, bool kPartial, bool kCross, class Jobs, bool kMx = false>
+//
+// kGather: row r of a tile (output row row_lo + r) takes its activation codes
+// and scales from source row gidx[row_lo + r] of qa / sa (clamped into
+// [0, src_rows)), so a gather of quantised rows (MoE dispatch) needs no copy.
+// The row indices of the next tile are loaded when that tile is picked, one
+// tile ahead, and turned into DMA offsets at the current tile's last step,
+// after the per-step vmcnt(0) waits have retired them (2-slot ring only).
+template <class C, bool kPartial, bool kCross, class Jobs, bool kMx = false, bool kGather = false>
 __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64_t lda,
                                            const float* __restrict__ sa, int64_t ld_sa,
                                            const uint8_t* __restrict__ qw, int64_t ldw,
                                            const float* __restrict__ sw, int sw_ld,
                                            uint16_t* __restrict__ y, int64_t ldy, float* __restrict__ part,
-                                           int N, int KB, Jobs& jobs, uint8_t* lds) {
+                                           int N, int KB, Jobs& jobs, uint8_t* lds,
+                                           const int32_t* __restrict__ gidx = nullptr, int src_rows = 0) {
   constexpr int S = C::STAGES;
   static_assert(S == 2 || !kCross, "the cross-tile pipeline is written for a 2-slot ring");
+  static_assert(!kGather || (S == 2 && kCross && !kPartial), "row gather: 2-slot cross-tile pipeline only");
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -233,16 +242,36 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
   //      logical chunk (L & 7) ^ swz_key(row) of the swizzled layout.  The
   //      per-lane byte offsets clamp rows past the tile's valid range.
   const int lrow = lane >> 3;
-  auto dma_offsets = [&](uint32_t (&g)[C::kLoadsPerWave], int n_valid, int m_valid) {
+  // (kGather: rs[i] is the source row of octet i's activation row; the offsets
+  // are then relative to qa itself rather than to the tile's first row)
+  auto dma_offsets = [&](uint32_t (&g)[C::kLoadsPerWave], int n_valid, int m_valid,
+                         const int32_t (&rs)[C::kLoadsPerWave]) {
 #pragma unroll
     for (int i = 0; i < C::kLoadsPerWave; ++i) {
       const int o = wave + i * C::kWaves;               // wave-uniform
       const bool w = o < C::BN / 8;
       const int r = (w ? o : o - C::BN / 8) * 8 + lrow;
       const int lchunk = (lane & 7) ^ swz_key(r);
+      const int arow = kGather ? rs[i] : min(r, m_valid - 1);
       g[i] = w ? (uint32_t)(min(r, n_valid - 1) * ldw + lchunk * 16)
-               : (uint32_t)(min(r, m_valid - 1) * lda + lchunk * 16);
+               : (uint32_t)(arow * lda + lchunk * 16);
     }
+  };
+  // kGather: issue the loads of a tile's source rows (octet rows and this
+  // lane's scale row); they are consumed a tile later
+  auto load_rows = [&](const TileJob& j, int32_t (&rs)[C::kLoadsPerWave], int32_t& srow) {
+#pragma unroll
+    for (int i = 0; i < C::kLoadsPerWave; ++i) {
+      const int o = wave + i * C::kWaves;
+      rs[i] = 0;
+      if (o >= C::BN / 8) rs[i] = gidx[j.row_lo + min((o - C::BN / 8) * 8 + lrow, j.m_valid - 1)];
+    }
+    srow = gidx[j.row_lo + min(wave * 64 + lane, j.m_valid - 1)];
+  };
+  auto clamp_rows = [&](int32_t (&rs)[C::kLoadsPerWave], int32_t& srow) {
+#pragma unroll
+    for (int i = 0; i < C::kLoadsPerWave; ++i) rs[i] = min(max(rs[i], 0), src_rows - 1);
+    srow = min(max(srow, 0), src_rows - 1);
   };
   // scales: wave w < kScaleLoads DMAs tokens 64w .. 64w+63 of the tile (clamped
   // to the last valid row); this wave's 128-row weight scale block is read with
@@ -256,33 +285,45 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
   TileJob nxt = cur;
   bool has_nxt = false;
   uint32_t goff[C::kLoadsPerWave], goff_n[C::kLoadsPerWave];
-  dma_offsets(goff, n_valid_of(cur), cur.m_valid);
+  int32_t rs_c[C::kLoadsPerWave] = {}, rs_n[C::kLoadsPerWave] = {};
+  int32_t srow_c = 0, srow_n = 0;
+  if constexpr (kGather) {
+    load_rows(cur, rs_c, srow_c);
+    clamp_rows(rs_c, srow_c);
+  }
+  dma_offsets(goff, n_valid_of(cur), cur.m_valid, rs_c);
   if constexpr (kCross) {
     has_nxt = jobs.next(nxt);
-    if (has_nxt) dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid);
+    if constexpr (kGather) {
+      if (has_nxt) load_rows(nxt, rs_n, srow_n);
+    } else {
+      if (has_nxt) dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid, rs_n);
+    }
   }
+  // this lane's activation-scale row of a tile (the scale DMA of waves < kScaleLoads)
+  auto sa_lane_cur = [&]() { return kGather ? sa + srow_c : sa_lane_of(cur); };
 
   // prologue: the first tile's first S-1 K blocks into slots 0 .. S-2
 #pragma unroll
   for (int p = 0; p < S - 1; ++p) {
     if (p > 0 && p >= KB) break;
     const uint8_t* wb = qw + cur.qw_off + (int64_t)cur.n0 * ldw + p * 128;
-    const uint8_t* ab = qa + (int64_t)cur.row_lo * lda + p * 128;
+    const uint8_t* ab = (kGather ? qa : qa + (int64_t)cur.row_lo * lda) + p * 128;
     uint8_t* ps = lds + p * C::kStageBytes;
 #pragma unroll
     for (int i = 0; i < C::kLoadsPerWave; ++i) {
       const int o = wave + i * C::kWaves;
       lds_dma16((o < C::BN / 8 ? wb : ab) + goff[i], ps + o * 1024);
     }
-    if (sdma) lds_dma4(sa_lane_of(cur) + (int64_t)p * ld_sa, ps + C::kWBytes + C::kABytes + wave * 256);
+    if (sdma) lds_dma4(sa_lane_cur() + (int64_t)p * ld_sa, ps + C::kWBytes + C::kABytes + wave * 256);
   }
 
   int slot = 0;
   for (;;) {
     const int n_valid = n_valid_of(cur);
     const uint8_t* wbase = qw + cur.qw_off + (int64_t)cur.n0 * ldw;
-    const uint8_t* abase = qa + (int64_t)cur.row_lo * lda;
-    const float* sa_lane = sa_lane_of(cur);
+    const uint8_t* abase = kGather ? qa : qa + (int64_t)cur.row_lo * lda;
+    const float* sa_lane = sa_lane_cur();
     const float* swrow = sw + cur.sw_off + (int64_t)(min(cur.n0 + wn * C::WTN, N - 1) >> 7) * sw_ld;
 
     v4f32 acc[C::TN][C::TM];
@@ -316,9 +357,19 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
       if constexpr (kCross) {
         if (last) {
           dwb = qw + nxt.qw_off + (int64_t)nxt.n0 * ldw;
-          dab = qa + (int64_t)nxt.row_lo * lda;
+          dab = kGather ? qa : qa + (int64_t)nxt.row_lo * lda;
           dsoff = 0;
-          dsa = sa_lane_of(nxt);
+          if constexpr (kGather) {
+            // the next tile's source rows, loaded a tile ago (retired by this
+            // step's vmcnt(0)): its DMA offsets and scale row
+            if (has_nxt) {
+              clamp_rows(rs_n, srow_n);
+              dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid, rs_n);
+            }
+            dsa = sa + srow_n;
+          } else {
+            dsa = sa_lane_of(nxt);
+          }
         }
       }
       const __amdgpu_buffer_rsrc_t rw = buffer_rsrc(dwb), ra = buffer_rsrc(dab);
@@ -462,7 +513,12 @@ __device__ __forceinline__ void gemm_tiles(const uint8_t* __restrict__ qa, int64
 #pragma unroll
       for (int i = 0; i < C::kLoadsPerWave; ++i) goff[i] = goff_n[i];
       has_nxt = jobs.next(nxt);
-      if (has_nxt) dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid);
+      if constexpr (kGather) {
+        srow_c = srow_n;
+        if (has_nxt) load_rows(nxt, rs_n, srow_n);
+      } else {
+        if (has_nxt) dma_offsets(goff_n, n_valid_of(nxt), nxt.m_valid, rs_n);
+      }
     }
   }
   // (the last step of the last tile issued no DMA: nothing is in flight here)

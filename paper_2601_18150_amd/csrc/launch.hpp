@@ -61,6 +61,15 @@ hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, in
                                           int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
                                           hipStream_t stream, bool pow2_scales);
 
+// The grouped GEMM over gathered rows: output row r uses activation row
+// row_index[r] of qa [src_rows][lda] and of sa [K/128][ld_sa] (indices clamped
+// into range); src_rows * lda < 2^32.
+hipError_t launch_grouped_gemm_w8a8_block_gathered(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                                   int64_t src_rows, const int32_t* row_index, const uint8_t* qw,
+                                                   const float* sw, const int32_t* group_offsets, int64_t num_groups,
+                                                   int64_t total_rows, uint16_t* y, int64_t n, int64_t k,
+                                                   hipStream_t stream);
+
 // Token-level TIS weights and mismatch-KL sums: workgroups of the first pass
 // (each leaves 4 doubles of partial sums in `partial`), then one that adds them.
 int tis_blocks(int64_t n);

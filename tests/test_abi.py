@@ -130,6 +130,22 @@ def test_gemm_argument_errors(lib):
     assert f(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None) == OK
 
 
+def test_grouped_gathered_argument_errors(lib):
+    f = lib.fp8rl_grouped_gemm_w8a8_block_gathered
+    #       qa  lda  sa  ld_sa src idx  qw   sw   off  g  rows y    n    k
+    assert f(A16, 128, A16, 8, 8, A16, A16, A16, A16, 2, -1, A16, 128, 128, None) == INVALID
+    assert f(A16, 128, A16, 8, 8, A16, A16, A16, A16, 0, 8, A16, 128, 128, None) == INVALID     # no groups
+    assert f(A16, 128, A16, 8, 8, A16, A16, A16, A16, 2, 8, A16, 200, 128, None) == SHAPE      # n % 128
+    assert f(A16, 128, A16, 8, 0, A16, A16, A16, A16, 2, 8, A16, 128, 128, None) == INVALID    # no tokens
+    assert f(A16, 128, A16, 8, 8, None, A16, A16, A16, 2, 8, A16, 128, 128, None) == INVALID   # no index
+    assert f(A16, 112, A16, 8, 8, A16, A16, A16, A16, 2, 8, A16, 128, 128, None) == INVALID    # lda < k
+    assert f(A16, 128, A16, 7, 8, A16, A16, A16, A16, 2, 8, A16, 128, 128, None) == INVALID    # ld_sa < src_rows
+    assert f(A16, 1 << 16, A16, 1 << 16, 1 << 16, A16, A16, A16, A16, 2, 8, A16, 128, 128, None) == SHAPE  # 2^32
+    assert f(A16, 136, A16, 8, 8, A16, A16, A16, A16, 2, 8, A16, 128, 128, None) == MISALIGNED  # lda % 16
+    assert f(A16, 128, A16, 8, 8, A16 + 2, A16, A16, A16, 2, 8, A16, 128, 128, None) == MISALIGNED
+    assert f(None, 128, None, 8, 8, None, None, None, None, 2, 0, None, 128, 128, None) == OK  # no rows: no-op
+
+
 def test_gemm_workspace_size(lib):
     """The split-K workspace is a pure function of the shape: splits x M x N fp32."""
     f = lib.fp8rl_gemm_w8a8_block_workspace_size

@@ -5,14 +5,19 @@ activations dynamically per token and 128-wide group).
 
 h is the correctly rounded bf16 of the exact value on both sides, so h, codes
 and scales are all compared bit for bit; codes and scales only where h is
-finite (NaN / inf activations are outside the quantiser's domain)."""
+finite (NaN / inf activations are outside the quantiser's domain).
+
+The grouped GEMM over gathered token rows (dispatch and expert product in one
+pass) is checked against the oracle's gathered product and bit for bit against
+the gather followed by the grouped GEMM."""
 import numpy as np
 import pytest
 import torch
 
 import synth
-from oracle import act, cref, quant
-from tests.gpu_util import announce, assert_codes_equal, assert_scales_equal, need_gpu, u8, u16, f32
+from oracle import act, cref, gemm, quant
+from tests.gpu_util import (announce, assert_codes_equal, assert_scales_equal, bf16_to_f64, need_gpu, u8, u16,
+                            f32)
 
 pytestmark = pytest.mark.gpu
 
@@ -220,3 +225,85 @@ def test_gather_then_gemm_equals_gemm_of_gathered_rows(fp8rl):
     q2, s2 = fp8rl.fp8rl_quant_act_token_group128(x[idx.long()].contiguous())
     torch.cuda.synchronize()
     assert torch.equal(gq, q2) and torch.equal(gs, s2)
+
+
+def _gathered_case(rng, t, counts, n, k, lda_pad=0, ldsa_pad=0):
+    """Token table [t][k] (oracle-quantised bf16 N(0,1) rows), expert weights, a
+    routing index with repeats and unused tokens."""
+    g = len(counts)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    r = int(offsets[-1])
+    a16 = torch.from_numpy(rng.standard_normal((t, k)).astype(np.float32)).to(torch.bfloat16)
+    w16 = torch.from_numpy((rng.standard_normal((g * n, k)) * 0.02).astype(np.float32)).to(torch.bfloat16)
+    qa, sa = cref.quant_act_token_group128(u16(a16))
+    qw, sw = cref.quant_weight_block128(u16(w16))
+    index = rng.integers(0, t, size=r).astype(np.int32)
+    qa_d = torch.zeros((t, k + lda_pad), dtype=torch.uint8, device="cuda")
+    qa_d[:, :k] = torch.from_numpy(qa).cuda()
+    sa_d = torch.zeros((k // 128, t + ldsa_pad), dtype=torch.float32, device="cuda")
+    sa_d[:, :t] = torch.from_numpy(sa).cuda()
+    dev = {"qa": qa_d[:, :k], "sa": sa_d, "index": torch.from_numpy(index).cuda(),
+           "qw": torch.from_numpy(qw.reshape(g, n, k)).cuda(),
+           "sw": torch.from_numpy(sw.reshape(g, n // 128, k // 128)).cuda(),
+           "offsets": torch.from_numpy(offsets).cuda()}
+    host = (qa, sa, index, qw.reshape(g, n, k), sw.reshape(g, n // 128, k // 128), offsets)
+    return dev, host
+
+
+@pytest.mark.parametrize("t,counts,n,k", [
+    (37, [5, 0, 130, 1, 0, 64], 384, 256),            # 256x128 tiles (K <= 1024)
+    (300, [257, 0, 3, 129], 256, 1152),               # 128x128 tiles (K > 1024)
+    (700, list(range(0, 400, 7)), 640, 384),          # > 512 tiles: several per persistent workgroup
+    (700, list(range(0, 400, 7)), 768, 1280),
+])
+def test_grouped_gathered_matches_oracle(fp8rl, t, counts, n, k):
+    """The grouped product over gathered token rows against the oracle: repeated and
+    unused tokens, empty and ragged experts, a token-table row pitch > K and ld_sa > T."""
+    announce(f"grouped gathered t={t} experts={len(counts)} n={n} k={k}")
+    rng = np.random.default_rng(t + n + k)
+    dev, host = _gathered_case(rng, t, counts, n, k, lda_pad=32, ldsa_pad=3)
+    y = fp8rl.fp8rl_grouped_gemm_w8a8_block_gathered(dev["qa"], dev["sa"], dev["index"], dev["qw"], dev["sw"],
+                                                     dev["offsets"])
+    torch.cuda.synchronize()
+    ref = gemm.grouped_gemm_gathered_ref_fp64(*host)
+    ok, worst, _ = gemm.tolerance_check(bf16_to_f64(y), ref)
+    assert ok, f"worst |err|/bound {worst:.3f}"
+
+
+@pytest.mark.parametrize("which", ["gate_up", "down"])
+def test_grouped_gathered_bit_identical_to_gather_then_grouped(fp8rl, which):
+    """Qwen3-30B-A3B expert shapes, 4096 tokens routed top-8 (Zipf loads, empty experts):
+    exactly the bits of fp8rl_gather_rows_fp8 followed by the grouped GEMM."""
+    announce(f"grouped gathered vs gather + grouped, MoE {which}")
+    lay = synth.moe_layer(device="cuda")
+    rt = lay["routing"]
+    off = rt.offsets.cuda()
+    idx = rt.token_of_row.to(torch.int32).cuda()
+    wts = lay["w_gate_up"] if which == "gate_up" else lay["w_down"]
+    g, n, k = wts.shape
+    tokens = synth.normal_bf16((4096, k), 1.0, 77, "cuda")
+    q, s = fp8rl.fp8rl_quant_act_token_group128(tokens)
+    qw, sw = fp8rl.fp8rl_quant_weight_block128(wts.reshape(g * n, k))
+    qw, sw = qw.reshape(g, n, k), sw.reshape(g, n // 128, k // 128)
+    y1 = fp8rl.fp8rl_grouped_gemm_w8a8_block_gathered(q, s, idx, qw, sw, off)
+    gq, gs = fp8rl.fp8rl_gather_rows_fp8(q, s, idx)
+    y2 = fp8rl.fp8rl_grouped_gemm_w8a8_block(gq, gs, qw, sw, off)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+def test_grouped_gathered_out_of_range_index_is_clamped(fp8rl):
+    """Indices outside [0, T) read the nearest valid token (never out of bounds)."""
+    announce("grouped gathered clamped indices")
+    rng = np.random.default_rng(9)
+    dev, host = _gathered_case(rng, 50, [40, 24], 256, 256)
+    bad = dev["index"].clone()
+    bad[::5] = 1000
+    bad[1::7] = -3
+    y = fp8rl.fp8rl_grouped_gemm_w8a8_block_gathered(dev["qa"], dev["sa"], bad, dev["qw"], dev["sw"],
+                                                     dev["offsets"])
+    good = bad.clamp(0, 49)
+    y2 = fp8rl.fp8rl_grouped_gemm_w8a8_block_gathered(dev["qa"], dev["sa"], good, dev["qw"], dev["sw"],
+                                                      dev["offsets"])
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))

@@ -118,6 +118,36 @@ def test_grouped_single_group_equals_dense():
     assert np.array_equal(y, gemm.gemm_ref_fp64(qa, sa, qw[0], sw[0]))
 
 
+def test_grouped_gathered_rows_bruteforce_and_composition():
+    """Rows taken from a token table by index (repeats, unused tokens, an empty expert):
+    each row equals the blockwise brute force on its token; the whole equals gathering
+    the quantised rows first and then the grouped product; the identity index gives
+    the grouped product itself."""
+    from oracle import act
+    rng = np.random.default_rng(6)
+    g, n, k, t = 3, 128, 256, 5
+    counts = [4, 0, 3]
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    r = int(offsets[-1])
+    index = np.array([4, 0, 4, 2, 1, 1, 3], np.int32)[:r]
+    qa = rand_codes((t, k), rng)
+    sa = rng.random((k // 128, t + 2)).astype(np.float32) + 0.5     # ld_sa > t
+    qw = rand_codes((g, n, k), rng)
+    sw = rng.random((g, n // 128, k // 128)).astype(np.float32) + 0.5
+    y = gemm.grouped_gemm_gathered_ref_fp64(qa, sa, index, qw, sw, offsets)
+    for e in range(g):
+        for row in range(offsets[e], offsets[e + 1]):
+            tok = index[row]
+            yb = gemm.gemm_blockwise_bruteforce(qa[tok:tok + 1], sa[:, tok:tok + 1], qw[e], sw[e])
+            assert np.allclose(y[row:row + 1], yb, rtol=1e-12, atol=1e-12 * np.abs(yb).max())
+    qg, sg = act.gather_rows_fp8(qa, sa[:, :t], index)
+    assert np.array_equal(y, gemm.grouped_gemm_ref_fp64(qg, sg, qw, sw, offsets))
+    ident = np.arange(t, dtype=np.int32)
+    off1 = np.array([0, 2, 2, t], np.int32)
+    assert np.array_equal(gemm.grouped_gemm_gathered_ref_fp64(qa, sa, ident, qw, sw, off1),
+                          gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, off1))
+
+
 def test_tolerance_check_semantics():
     ref = np.array([[1.0, -2.0], [0.0, 4.0]])
     rms = np.sqrt(np.mean(ref ** 2))
