@@ -143,10 +143,11 @@ int fp8rl_gemm_w8a8_block(const uint8_t* qa, int64_t lda, const float* sa, int64
 /*
  * The same dense product (same operation and arguments as fp8rl_gemm_w8a8_block,
  * section 2.1.1 Eq. (1) and section 2.1.4), for callers that can lend a
- * workspace: shapes whose 128 x 128 output tiles are too few to fill the GPU
- * (decode, m of a few hundred tokens) split the K range over several workgroups,
- * which write fp32 partial sums to the workspace; a second kernel adds them in
- * a fixed order and rounds to bf16 once.
+ * workspace: shapes whose output tiles are too few to fill the GPU (decode,
+ * m of up to a few hundred tokens; for 128 < m <= 256 only when k > 4096, as
+ * shorter K ranges run unsplit on 64 x 64 tiles) split the K range over several
+ * workgroups, which write fp32 partial sums to the workspace; a second kernel
+ * adds them in a fixed order and rounds to bf16 once.
  *
  * fp8rl_gemm_w8a8_block_workspace_size: bytes of workspace the split needs for
  * this shape (splits * m * n * 4), 0 when the shape is not split (then
