@@ -98,6 +98,9 @@ def test_quant_weight_batched_argument_errors(lib):
             assert f(p, len(specs), None) == code, (specs, code)
     p, keep = jobs((A16, 0, 128, 128, A16, 128, A16), (None, 0, 0, 0, None, 0, None))
     assert f(p, 2, None) == OK                                           # only empty jobs: no-op
+    # a bad job in the second 64-job chunk: rejected before the first chunk launches
+    p, keep = jobs(*([good] * 69 + [(A16, 128, 128, 128, A16, 136, A16)]))
+    assert f(p, 70, None) == MISALIGNED
 
 
 def test_quant_act_argument_errors(lib):
