@@ -6,7 +6,10 @@
 //    the spec peak;
 //  * the fp32 fast path of the SiLU * up evaluation (silu_math.hpp, the same
 //    code the fused down-projection kernel runs) element by element, so that
-//    its error can be measured against the exact value for every input.
+//    its error can be measured against the exact value for every input;
+//  * single v_mfma_f32_16x16x128_f8f6f4 instructions on operands given by the
+//    host, so that the instruction's summation of its 128 products (and of the
+//    accumulator input) can be compared with the exact sums.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -57,7 +60,42 @@ __global__ __launch_bounds__(256) void silu_fast_kernel(const uint16_t* __restri
   q[i] = qi;
 }
 
+// One wave per case: d = c + A . B^T for one 16x16x128 E4M3 tile, computed by
+// exactly one v_mfma_f32_16x16x128_f8f6f4.  a, b: [cases][16][128] codes (row i
+// of A, row j of B); c, d: [cases][16][16] fp32, element [i][j].  Lane L feeds
+// row L % 16 of each operand, K bytes 32 (L / 16) .. +31, and holds the results
+// [4 (L / 16) + r][L % 16], r = 0..3.
+__global__ __launch_bounds__(64) void mfma_tile_kernel(const uint8_t* __restrict__ a, const uint8_t* __restrict__ b,
+                                                       const float* __restrict__ c, float* __restrict__ d) {
+  const int64_t cs = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int row = lane & 15, g = lane >> 4;
+  const uint4* pa = reinterpret_cast<const uint4*>(a + cs * 2048 + row * 128 + g * 32);
+  const uint4* pb = reinterpret_cast<const uint4*>(b + cs * 2048 + row * 128 + g * 32);
+  const uint4 a0 = pa[0], a1 = pa[1], b0 = pb[0], b1 = pb[1];
+  v8i32 fa, fb;
+  fa[0] = (int)a0.x; fa[1] = (int)a0.y; fa[2] = (int)a0.z; fa[3] = (int)a0.w;
+  fa[4] = (int)a1.x; fa[5] = (int)a1.y; fa[6] = (int)a1.z; fa[7] = (int)a1.w;
+  fb[0] = (int)b0.x; fb[1] = (int)b0.y; fb[2] = (int)b0.z; fb[3] = (int)b0.w;
+  fb[4] = (int)b1.x; fb[5] = (int)b1.y; fb[6] = (int)b1.z; fb[7] = (int)b1.w;
+  v4f32 acc;
+  for (int r = 0; r < 4; ++r) acc[r] = c[cs * 256 + (4 * g + r) * 16 + row];
+  acc = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(fa, fb, acc, 0, 0, 0, 0, 0, 0);
+  for (int r = 0; r < 4; ++r) d[cs * 256 + (4 * g + r) * 16 + row] = acc[r];
+}
+
 }  // namespace
+
+// a, b: cases x 2048 codes; c, d: cases x 256 floats (device pointers, 16-byte
+// aligned).  0 on success, 1 for a bad argument, 4 for a launch error.
+extern "C" int fp8rl_probe_mfma_tile(const uint8_t* a, const uint8_t* b, const float* c, float* d, long long cases,
+                                     void* stream) {
+  if (cases < 0 || cases >= (1ll << 31) || (cases > 0 && (!a || !b || !c || !d))) return 1;
+  if (cases == 0) return 0;
+  hipLaunchKernelGGL(mfma_tile_kernel, dim3((unsigned)cases), dim3(64), 0, static_cast<hipStream_t>(stream), a, b, c,
+                     d);
+  return hipGetLastError() == hipSuccess ? 0 : 4;
+}
 
 // Enqueue the probe: `blocks` workgroups of 256 threads; out holds blocks*256
 // floats, clk 2*blocks counters (device pointers).  Returns a hipError_t value.

@@ -3,14 +3,15 @@ fp64 oracle on the same FP8 codes and scales.
 
 Codes and scales given to the GPU are made by the oracle (or drawn directly as
 random codes), never by the GPU quantisers.  Pass criterion per element:
-|gpu - ref| <= 4e-3 |ref| + 1e-3 rms(ref), rms over the call's output (over the
-sampled rows where the output is only sampled)."""
+|gpu - ref| <= 4e-3 |ref| + 1e-3 rms(ref), rms over the call's whole output; every
+output element of every call is compared."""
 import numpy as np
 import pytest
 import torch
 
 import synth
 from oracle import cref, gemm
+from tests import mfma_model
 from tests.gpu_util import announce, bf16_to_f64, need_gpu, u16
 
 pytestmark = pytest.mark.gpu
@@ -39,22 +40,66 @@ def rand_scales(shape, rng):
     return (2.0 ** rng.uniform(-12, -2, size=shape)).astype(np.float32)
 
 
-def check(y_gpu: torch.Tensor, y_ref: np.ndarray, what: str, rows=None):
+def check(y_gpu: torch.Tensor, y_ref: np.ndarray, what: str, attribute=None, budget=0):
+    """Every element within |gpu - ref| <= 4e-3 |ref| + 1e-3 rms(ref) of the fp64 oracle.
+
+    The FP8 MFMA truncates products that share a group of 8 K positions with a much
+    larger one (tests/test_gpu_mfma_precision.py), so on operands with large in-block
+    dynamic range a few elements can miss that tolerance whatever the kernel does.
+    Such elements are allowed only where a test names a budget: at most `budget` of
+    them, and each must equal, within the same tolerance, `attribute(rows, cols)`:
+    the kernel's arithmetic emulated with the instruction's measured summation
+    (tests/mfma_model.py)."""
     got = bf16_to_f64(y_gpu)
-    if rows is not None:
-        got = got[rows]
     ok, worst, rms = gemm.tolerance_check(got, y_ref)
-    if not ok:
-        err = np.abs(got - y_ref)
-        ratio = err / (4e-3 * np.abs(y_ref) + 1e-3 * rms)
-        order = np.argsort(ratio, axis=None)[::-1][:5]
-        lines = []
-        for flat in order:
-            idx = np.unravel_index(flat, ratio.shape)
-            lines.append(f"  at {tuple(int(i) for i in idx)}: gpu {got[idx]!r} ref {y_ref[idx]!r} "
-                         f"err {err[idx]:.4g} ratio {ratio[idx]:.3f}")
-        print("\n".join(lines))
-    assert ok, f"{what}: worst |err|/bound = {worst:.3f} (rms {rms:.4g})"
+    if ok:
+        return
+    bound = 4e-3 * np.abs(y_ref) + 1e-3 * rms
+    err = np.abs(got - y_ref)
+    bad = np.nonzero(err > bound)
+    nbad = bad[0].size
+    ratio = err[bad] / bound[bad]
+    for t in np.argsort(ratio)[::-1][:5]:
+        idx = tuple(int(b[t]) for b in bad)
+        print(f"  at {idx}: gpu {got[idx]!r} ref {y_ref[idx]!r} err {err[idx]:.4g} ratio {ratio[t]:.3f}")
+    assert attribute is not None and nbad <= budget, \
+        f"{what}: {nbad} elements outside the tolerance, worst |err|/bound = {worst:.3f} (rms {rms:.4g})"
+    emu = attribute(*bad)
+    off_model = np.abs(got[bad] - emu) > bound[bad]
+    assert not off_model.any(), f"{what}: {int(off_model.sum())} of {nbad} elements outside the tolerance are " \
+        "not the instruction's summation either"
+    print(f"{what}: {nbad} of {y_ref.size} elements outside the tolerance against the fp64 oracle (worst ratio "
+          f"{worst:.3f}), each equal to the emulated FP8 MFMA summation within it")
+
+
+def dense_attribution(qa, sa, qw, sw, pow2_scales=False):
+    """attribute() for check(): the dense kernel emulated with the instruction model."""
+    def emulate(rows, cols):
+        return mfma_model.gemm_elements(qa[rows], np.asarray(sa)[:, rows].T, qw[cols], np.asarray(sw)[cols // 128],
+                                        pow2_scales)
+    return emulate
+
+
+def grouped_attribution(qa, sa, qw, sw, offsets, pow2_scales=False):
+    """attribute() for check(): the grouped kernel emulated per element with its expert's weights."""
+    def emulate(rows, cols):
+        e = np.searchsorted(np.asarray(offsets), rows, side="right") - 1
+        return mfma_model.gemm_elements(qa[rows], np.asarray(sa)[:, rows].T, qw[e, cols], sw[e, cols // 128],
+                                        pow2_scales)
+    return emulate
+
+
+def dense_ref_by_rows(qa, sa, qw, sw, chunk=1024):
+    """The oracle's dense product (dequantise, then an fp64 matmul), evaluated over
+    row chunks so that the dequantised weight is formed once: row for row the same
+    numbers as gemm.gemm_ref_fp64."""
+    wd_t = np.ascontiguousarray(gemm.dequant_weight(qw, sw).T)
+    m = qa.shape[0]
+    ref = np.empty((m, qw.shape[0]), np.float64)
+    for r0 in range(0, m, chunk):
+        r1 = min(m, r0 + chunk)
+        np.matmul(gemm.dequant_act(qa[r0:r1], sa[:, r0:r1]), wd_t, out=ref[r0:r1])
+    return ref
 
 
 def run_dense(fp8rl, qa, sa, qw, sw, lda_pad=0, ldy_pad=0, ldsa_pad=0):
@@ -149,36 +194,19 @@ def test_gemm_largest_row_pitch(fp8rl, m, n, k):
     check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), f"pitch {pitch} {m}x{n}x{k}")
 
 
-def test_gemm_full_range_codes_within_accumulation_bound(fp8rl):
-    """Uniformly random codes over the whole E4M3 range (products up to 448^2 with
-    heavy cancellation inside a K block).
-
-    Measured on gfx950: the FP8 MFMA sums the 128 products of one instruction
-    with less than fp32 precision (errors up to about 2^-14 of the block's
-    absolute product sum), so on such inputs a few elements whose value is far
-    below their partial sums miss the 4e-3/1e-3 tolerance.  This test bounds the
-    error by bf16 rounding plus 2^-12 of each block's scaled absolute product sum,
-    and reports how many elements fall outside the plain tolerance."""
-    announce("gemm full-range random codes, accumulation bound")
+def test_gemm_full_range_codes(fp8rl):
+    """Uniformly random codes over the whole E4M3 range: products from 2^-18 to 448^2 in
+    every K group, with heavy cancellation.  The stated tolerance against the fp64
+    oracle on every element, except a budgeted handful where the FP8 MFMA's own
+    summation (products truncated below the largest one of their group of 8,
+    tests/test_gpu_mfma_precision.py) is what misses it."""
+    announce("gemm full-range random codes")
     rng = np.random.default_rng(2048 * 7 + 2048 + 256)
     m, n, k = 2048, 2048, 256
     qa, qw = rand_codes((m, k), rng), rand_codes((n, k), rng)
     sa, sw = rand_scales((k // 128, m), rng), rand_scales((n // 128, k // 128), rng)
-    y = bf16_to_f64(run_dense(fp8rl, qa, sa, qw, sw))
-    ref = gemm.gemm_ref_fp64(qa, sa, qw, sw)
-    from oracle import e4m3
-    da, dw = np.abs(e4m3.decode(qa)), np.abs(e4m3.decode(qw))
-    abs_sum = np.zeros((m, n))
-    for kb in range(k // 128):
-        sl = slice(kb * 128, (kb + 1) * 128)
-        blk = da[:, sl] @ dw[:, sl].T
-        abs_sum += blk * sa[kb][:, None] * np.repeat(sw[:, kb], 128)[None, :]
-    err = np.abs(y - ref)
-    bound = 2.0 ** -8 * np.abs(ref) * (1 + 2.0 ** -8) + 2.0 ** -12 * abs_sum
-    assert np.all(err <= bound), f"worst err/bound {np.max(err / bound):.3f}"
-    ok, worst, rms = gemm.tolerance_check(y, ref)
-    outside = int(np.sum(err > 4e-3 * np.abs(ref) + 1e-3 * rms))
-    print(f"full-range codes: {outside} of {m * n} elements outside the plain tolerance (worst {worst:.3f})")
+    y = run_dense(fp8rl, qa, sa, qw, sw)
+    check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), "full-range codes", dense_attribution(qa, sa, qw, sw), budget=16)
 
 
 def test_gemm_k_block_accumulates_in_fp32(fp8rl):
@@ -287,18 +315,18 @@ def test_gemm_split_k_short_workspace_runs_unsplit(fp8rl):
     assert torch.equal(y_ws.view(torch.int16), y.view(torch.int16))
 
 
-def test_gemm_prefill_full_size_sampled_rows(fp8rl):
-    """8192x4096 -> 24576 with outliers: the full GEMM on the GPU, the oracle on sampled rows."""
-    announce("gemm prefill 8192x4096x24576")
+def test_gemm_prefill_full_size_every_element(fp8rl):
+    """8192x4096 -> 24576 with outliers: the full GEMM on the GPU against the fp64 oracle
+    on every one of its 201M outputs (the oracle runs over row chunks of the same
+    codes and scales; rms over the whole output)."""
+    announce("gemm prefill 8192x4096x24576, every element")
     a, w = synth.prefill_linear()
     qa, sa = cref.quant_act_token_group128(u16(a))
     qw, sw = cref.quant_weight_block128(u16(w))
     y = run_dense(fp8rl, qa, sa, qw, sw)
-    rng = np.random.default_rng(0)
-    rows = np.unique(np.concatenate([np.arange(8), np.arange(8184, 8192),
-                                     rng.choice(8192, 48, replace=False)]))
-    ref = gemm.gemm_ref_fp64(qa[rows], sa[:, rows], qw, sw)
-    check(y, ref, "prefill", rows=rows)
+    # 1% of the activation channels x50 and 0.1% of the weights x20 put very large and
+    # small products into one K group: a few elements carry the instruction's truncation
+    check(y, dense_ref_by_rows(qa, sa, qw, sw), "prefill", dense_attribution(qa, sa, qw, sw), budget=32)
 
 
 def test_gemm_deterministic(fp8rl):
@@ -382,9 +410,10 @@ def test_grouped_many_tiles_per_workgroup(fp8rl, k):
 
 
 @pytest.mark.parametrize("which", ["gate_up", "down"])
-def test_grouped_moe_full_size_sampled_rows(fp8rl, which):
-    """Qwen3-30B-A3B-shaped experts, Zipf(1.1) top-8 routing of 4096 tokens (some experts empty)."""
-    announce(f"grouped gemm MoE {which}")
+def test_grouped_moe_full_size_every_element(fp8rl, which):
+    """Qwen3-30B-A3B-shaped experts, Zipf(1.1) top-8 routing of 4096 tokens (some experts
+    empty): every row of every expert against the fp64 oracle."""
+    announce(f"grouped gemm MoE {which}, every element")
     moe = synth.moe_layer()
     off = moe["routing"].offsets.numpy()
     x = moe["x_gate_up"] if which == "gate_up" else moe["x_down"]
@@ -396,17 +425,8 @@ def test_grouped_moe_full_size_sampled_rows(fp8rl, which):
     sw = sw.reshape(g, n // 128, k // 128)
     assert (np.diff(off) == 0).sum() >= 8, "the workload is meant to have empty experts"
     y = run_grouped(fp8rl, qa, sa, qw, sw, off)
-    # oracle on the first, last and a middle row of every non-empty expert
-    rows, ref_rows = [], []
-    for e in range(g):
-        lo, hi = int(off[e]), int(off[e + 1])
-        if hi <= lo:
-            continue
-        pick = sorted({lo, hi - 1, (lo + hi) // 2})
-        ref = gemm.gemm_ref_fp64(qa[pick], sa[:, pick], qw[e], sw[e])
-        rows += pick
-        ref_rows.append(ref)
-    check(y, np.concatenate(ref_rows), f"moe {which}", rows=np.array(rows))
+    check(y, gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, off), f"moe {which}",
+          grouped_attribution(qa, sa, qw, sw, off), budget=8)
 
 
 def test_linear_w8a8_end_to_end_tiny(fp8rl):

@@ -10,7 +10,7 @@ import torch
 import synth
 from oracle import cref, gemm, ue8m0
 from tests.gpu_util import announce, assert_codes_equal, assert_scales_equal, need_gpu, u8, u16, f32
-from tests.test_gpu_gemm import check, to_dev
+from tests.test_gpu_gemm import check, dense_attribution, dense_ref_by_rows, grouped_attribution, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -150,15 +150,13 @@ def test_gemm_ue8m0_scale_per_operand_row_and_k_block(fp8rl):
     check(y, gemm.gemm_ref_fp64(qa, sa, qw, sw), "ue8m0 exact exponents")
 
 
-def test_gemm_ue8m0_prefill_full_size_sampled_rows(fp8rl):
-    announce("gemm_ue8m0 prefill 8192x4096x24576")
+def test_gemm_ue8m0_prefill_full_size_every_element(fp8rl):
+    announce("gemm_ue8m0 prefill 8192x4096x24576, every element")
     a, w = synth.prefill_linear()
     qa, sa = cref.quant_act_token_group128_ue8m0(u16(a))
     qw, sw = cref.quant_weight_block128_ue8m0(u16(w))
     y = run_dense_ue8m0(fp8rl, qa, sa, qw, sw)
-    rng = np.random.default_rng(0)
-    rows = np.unique(np.concatenate([np.arange(8), np.arange(8184, 8192), rng.choice(8192, 48, replace=False)]))
-    check(y, gemm.gemm_ref_fp64(qa[rows], sa[:, rows], qw, sw), "ue8m0 prefill", rows=rows)
+    check(y, dense_ref_by_rows(qa, sa, qw, sw), "ue8m0 prefill", dense_attribution(qa, sa, qw, sw, True), budget=32)
 
 
 def test_gemm_ue8m0_deterministic(fp8rl):
@@ -185,8 +183,8 @@ def test_grouped_ue8m0_small(fp8rl, counts):
 
 
 @pytest.mark.parametrize("which", ["gate_up", "down"])
-def test_grouped_ue8m0_moe_full_size_sampled_rows(fp8rl, which):
-    announce(f"grouped_ue8m0 MoE {which}")
+def test_grouped_ue8m0_moe_full_size_every_element(fp8rl, which):
+    announce(f"grouped_ue8m0 MoE {which}, every element")
     moe = synth.moe_layer()
     off = moe["routing"].offsets.numpy()
     x = moe["x_gate_up"] if which == "gate_up" else moe["x_down"]
@@ -197,12 +195,5 @@ def test_grouped_ue8m0_moe_full_size_sampled_rows(fp8rl, which):
     qw, sw = qw.reshape(g, n, k), sw.reshape(g, n // 128, k // 128)
     y = fp8rl.fp8rl_grouped_gemm_w8a8_block_ue8m0(to_dev(qa), to_dev(sa), to_dev(qw), to_dev(sw), to_dev(off))
     torch.cuda.synchronize()
-    rows, ref_rows = [], []
-    for e in range(g):
-        lo, hi = int(off[e]), int(off[e + 1])
-        if hi <= lo:
-            continue
-        pick = sorted({lo, hi - 1, (lo + hi) // 2})
-        ref_rows.append(gemm.gemm_ref_fp64(qa[pick], sa[:, pick], qw[e], sw[e]))
-        rows += pick
-    check(y, np.concatenate(ref_rows), f"moe ue8m0 {which}", rows=np.array(rows))
+    check(y, gemm.grouped_gemm_ref_fp64(qa, sa, qw, sw, off), f"moe ue8m0 {which}",
+          grouped_attribution(qa, sa, qw, sw, off, True), budget=8)
