@@ -52,7 +52,8 @@ typedef enum {
   FP8RL_ERR_INVALID_ARG = 1,       /* null pointer with nonzero size, negative size, ld too small, num_groups < 1 */
   FP8RL_ERR_UNSUPPORTED_SHAPE = 2, /* K or N not a multiple of 128, or a size beyond 2^31 elements per row/col */
   FP8RL_ERR_MISALIGNED = 3,        /* a pointer or leading dimension breaks the alignment rules stated below */
-  FP8RL_ERR_HIP = 4                /* the HIP runtime reported an error at launch */
+  FP8RL_ERR_HIP = 4,               /* the HIP runtime reported an error at launch */
+  FP8RL_ERR_SCRATCH_LIMIT = 5      /* the call needs more than the library's static scratch (no-allocation entry point) */
 } fp8rl_status;
 
 /*
@@ -170,6 +171,29 @@ int fp8rl_gemm_w8a8_block_ws(const uint8_t* qa, int64_t lda, const float* sa, in
                              const uint8_t* qw, int64_t ldw, const float* sw,
                              uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,
                              void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
+ * For callers that cannot allocate (code under HIP graph capture, serving loops
+ * that forbid allocation): the dense product of fp8rl_gemm_w8a8_block_ws without
+ * a workspace argument.  The split-K partial sums go to a static device array of
+ * FP8RL_SPLITK_SCRATCH_BYTES (16 MiB) inside the library, one per GPU, held
+ * until the process ends; its address on the current device is looked up once
+ * (hipGetSymbolAddress) and the call itself allocates nothing.  Same arguments,
+ * validation and result as fp8rl_gemm_w8a8_block_ws given a workspace of
+ * fp8rl_gemm_w8a8_block_workspace_size(m, n, k) bytes (bit-identical output).
+ * FP8RL_ERR_SCRATCH_LIMIT (nothing launched) when that size exceeds the static
+ * array; with the current split rule no valid shape needs more than 16 MiB.
+ * The array keeps the last call's contents and needs no clearing (every partial
+ * sum read is written first by the same call).  Calls that overlap in time on
+ * one GPU (concurrent streams or threads) share the array and race: serialise
+ * them.
+ */
+#define FP8RL_SPLITK_SCRATCH_BYTES (16ll << 20)
+
+int fp8rl_gemm_w8a8_block_noalloc(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa,
+                                  const uint8_t* qw, int64_t ldw, const float* sw,
+                                  uint16_t* y, int64_t ldy, int64_t m, int64_t n, int64_t k,
+                                  void* stream);
 
 /*
  * Grouped (MoE expert) blockwise-scaled FP8 GEMM (section 2.1.1: MoE expert

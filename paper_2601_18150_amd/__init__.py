@@ -23,7 +23,7 @@ __all__ = [
     "LIB_PATH", "Fp8rlError", "load",
     "fp8rl_quant_weight_block128", "fp8rl_quant_weight_block128_batched", "fp8rl_quant_act_token_group128",
     "fp8rl_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block", "fp8rl_grouped_gemm_w8a8_block_gathered",
-    "fp8rl_gemm_w8a8_block_workspace_size", "fp8rl_gemm_w8a8_block_ws",
+    "fp8rl_gemm_w8a8_block_workspace_size", "fp8rl_gemm_w8a8_block_ws", "fp8rl_gemm_w8a8_block_noalloc",
     "fp8rl_quant_weight_block128_ue8m0", "fp8rl_quant_act_token_group128_ue8m0",
     "fp8rl_gemm_w8a8_block_ue8m0", "fp8rl_grouped_gemm_w8a8_block_ue8m0",
     "fp8rl_silu_mul_quant_group128", "fp8rl_gather_rows_fp8",
@@ -38,7 +38,7 @@ __all__ = [
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfp8rl.so")
 
 _STATUS = {0: "FP8RL_OK", 1: "FP8RL_ERR_INVALID_ARG", 2: "FP8RL_ERR_UNSUPPORTED_SHAPE",
-           3: "FP8RL_ERR_MISALIGNED", 4: "FP8RL_ERR_HIP"}
+           3: "FP8RL_ERR_MISALIGNED", 4: "FP8RL_ERR_HIP", 5: "FP8RL_ERR_SCRATCH_LIMIT"}
 
 
 class Fp8rlError(RuntimeError):
@@ -69,6 +69,7 @@ def _load():
         "fp8rl_grouped_gemm_w8a8_block": [P, P, I, P, P, P, I, I, P, I, I, P],
         "fp8rl_grouped_gemm_w8a8_block_gathered": [P, I, P, I, I, P, P, P, P, I, I, P, I, I, P],
         "fp8rl_gemm_w8a8_block_ws": [P, I, P, I, P, I, P, P, I, I, I, I, P, I, P],
+        "fp8rl_gemm_w8a8_block_noalloc": [P, I, P, I, P, I, P, P, I, I, I, I, P],
         "fp8rl_quant_weight_block128_ue8m0": [P, I, I, I, P, I, P, P],
         "fp8rl_quant_act_token_group128_ue8m0": [P, I, I, I, P, I, P, I, P],
         "fp8rl_gemm_w8a8_block_ue8m0": [P, I, P, I, P, I, P, P, I, I, I, I, P],
@@ -332,6 +333,20 @@ def fp8rl_gemm_w8a8_block_ws(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tenso
                                       _ld(qw), sw.data_ptr(), y.data_ptr(), _ld(y), m, n, k,
                                       workspace.data_ptr(), nbytes, _stream(stream))
     _check("fp8rl_gemm_w8a8_block_ws", st)
+    return y
+
+
+def fp8rl_gemm_w8a8_block_noalloc(qa: torch.Tensor, sa: torch.Tensor, qw: torch.Tensor, sw: torch.Tensor,
+                                  y: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """fp8rl_gemm_w8a8_block_ws with the split-K partial sums in the library's static
+    device scratch instead of a workspace (the C call allocates nothing; pass y to
+    keep the wrapper from allocating the output)."""
+    qa, qw, y, m, n, k = _dense_args(qa, sa, qw, sw, y)
+    if m == 0:
+        return y
+    st = load().fp8rl_gemm_w8a8_block_noalloc(qa.data_ptr(), _ld(qa), sa.data_ptr(), sa.stride(0), qw.data_ptr(),
+                                              _ld(qw), sw.data_ptr(), y.data_ptr(), _ld(y), m, n, k, _stream(stream))
+    _check("fp8rl_gemm_w8a8_block_noalloc", st)
     return y
 
 

@@ -50,6 +50,7 @@ const char* fp8rl_status_string(int status) {
     case FP8RL_ERR_UNSUPPORTED_SHAPE: return "FP8RL_ERR_UNSUPPORTED_SHAPE";
     case FP8RL_ERR_MISALIGNED: return "FP8RL_ERR_MISALIGNED";
     case FP8RL_ERR_HIP: return "FP8RL_ERR_HIP";
+    case FP8RL_ERR_SCRATCH_LIMIT: return "FP8RL_ERR_SCRATCH_LIMIT";
     default: return "FP8RL_ERR_UNKNOWN";
   }
 }
@@ -201,6 +202,25 @@ int fp8rl_gemm_w8a8_block_ws(const uint8_t* qa, int64_t lda, const float* sa, in
     return hip_status(fp8rl::launch_gemm_w8a8_block_splitk(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k,
                                                            static_cast<float*>(workspace), splits,
                                                            as_stream(stream)));
+  return hip_status(
+      fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream), false));
+}
+
+static_assert(FP8RL_SPLITK_SCRATCH_BYTES == fp8rl::kSplitKScratchBytes, "header and library scratch sizes differ");
+
+int fp8rl_gemm_w8a8_block_noalloc(const uint8_t* qa, int64_t lda, const float* sa, int64_t ld_sa, const uint8_t* qw,
+                                  int64_t ldw, const float* sw, uint16_t* y, int64_t ldy, int64_t m, int64_t n,
+                                  int64_t k, void* stream) {
+  const int st = check_dense(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k);
+  if (st != kLaunch) return st;
+  const int splits = fp8rl::splitk_factor(m, n, k);
+  if (splits > 1) {
+    if (int64_t(splits) * m * n * 4 > fp8rl::kSplitKScratchBytes) return FP8RL_ERR_SCRATCH_LIMIT;
+    float* part = nullptr;
+    if (fp8rl::splitk_scratch(&part) != hipSuccess) return FP8RL_ERR_HIP;
+    return hip_status(fp8rl::launch_gemm_w8a8_block_splitk(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, part,
+                                                           splits, as_stream(stream)));
+  }
   return hip_status(
       fp8rl::launch_gemm_w8a8_block(qa, lda, sa, ld_sa, qw, ldw, sw, y, ldy, m, n, k, as_stream(stream), false));
 }

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "gemm_core.hpp"
 #include "launch.hpp"
 
@@ -358,6 +360,34 @@ hipError_t launch_gemm_w8a8_block_splitk(const uint8_t* qa, int64_t lda, const f
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, stream, part, m,
                      n, splits, y, ldy);
   return hipGetLastError();
+}
+
+// Split-K partial sums for callers that cannot allocate: a file-scope device
+// array (each GPU the library runs on holds its own copy until the process
+// ends).  In host code `scratch` only names the symbol; its device address on
+// the current device comes from hipGetSymbolAddress, fetched once per device.
+static __device__ __align__(256) float scratch[kSplitKScratchBytes / 4];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<float*> scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t splitk_scratch(float** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  float* p = scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    void* q = nullptr;
+    e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    p = static_cast<float*>(q);
+    scratch_ptr[dev].store(p, std::memory_order_release);   // racing first calls store the same address
+  }
+  *out = p;
+  return hipSuccess;
 }
 
 hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,

@@ -55,6 +55,13 @@ hipError_t launch_gemm_w8a8_block_splitk(const uint8_t* qa, int64_t lda, const f
                                          int64_t ldy, int64_t m, int64_t n, int64_t k, float* part, int splits,
                                          hipStream_t stream);
 
+// Device address, on the current device, of the library's static split-K
+// scratch (kSplitKScratchBytes); fetched once per device, no allocation.  The
+// split rule keeps splits * m * n <= 256 * 128 * 128 floats, so every split
+// shape fits.
+constexpr int64_t kSplitKScratchBytes = int64_t(16) << 20;
+hipError_t splitk_scratch(float** out);
+
 hipError_t launch_grouped_gemm_w8a8_block(const uint8_t* qa, const float* sa, int64_t ld_sa,
                                           const uint8_t* qw, const float* sw,
                                           const int32_t* group_offsets, int64_t num_groups,

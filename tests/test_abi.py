@@ -52,6 +52,7 @@ def test_status_strings_and_version(lib):
     import paper_2601_18150_amd as fp8rl
     assert fp8rl.fp8rl_status_string(0) == "FP8RL_OK"
     assert fp8rl.fp8rl_status_string(3) == "FP8RL_ERR_MISALIGNED"
+    assert fp8rl.fp8rl_status_string(5) == "FP8RL_ERR_SCRATCH_LIMIT"
     assert fp8rl.fp8rl_status_string(99) == "FP8RL_ERR_UNKNOWN"
     assert fp8rl.fp8rl_version() >= 100
 
@@ -174,6 +175,38 @@ def test_gemm_ws_argument_errors(lib):
     assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, A16 + 4, 64, None) == MISALIGNED
     assert f(A16 + 8, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, A16, 64, None) == MISALIGNED
     assert f(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None, 0, None) == OK
+
+
+def test_gemm_noalloc_argument_errors(lib):
+    """The no-allocation entry point validates exactly like the dense GEMM, before any device call."""
+    f = lib.fp8rl_gemm_w8a8_block_noalloc
+    #      qa  lda  sa  ld_sa qw  ldw  sw  y   ldy  m  n    k
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 200, 8, 200, 128, None) == SHAPE
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 192, None) == SHAPE
+    assert f(A16, 128, A16, 8, A16, 128, A16, A16, 128, -1, 128, 128, None) == INVALID
+    assert f(A16, 100, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == INVALID
+    assert f(A16, 128, A16, 4, A16, 128, A16, A16, 128, 8, 128, 128, None) == INVALID
+    assert f(None, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == INVALID
+    assert f(A16 + 8, 128, A16, 8, A16, 128, A16, A16, 128, 8, 128, 128, None) == MISALIGNED
+    assert f(A16, 128, A16, 8, A16, 1 << 24, A16, A16, 128, 8, 128, 128, None) == SHAPE
+    assert f(None, 128, None, 0, None, 128, None, None, 128, 0, 128, 128, None) == OK
+
+
+def test_split_k_partials_fit_the_static_scratch(lib):
+    """Every shape the split rule splits needs at most FP8RL_SPLITK_SCRATCH_BYTES (16 MiB) of partial
+    sums (splits x tiles <= 256 tiles of 128 x 128), so the no-allocation entry point never
+    returns FP8RL_ERR_SCRATCH_LIMIT for a valid shape; the worst case is reached exactly."""
+    f = lib.fp8rl_gemm_w8a8_block_workspace_size
+    text = open(HEADER).read()
+    limit = int(re.search(r"#define FP8RL_SPLITK_SCRATCH_BYTES \((\d+)ll << (\d+)\)", text).group(1)) << 20
+    assert limit == 16 << 20
+    worst = 0
+    for m in list(range(1, 300, 7)) + [128, 256, 384, 511, 512, 1024, 2047, 4096]:
+        for n in (128, 256, 384, 640, 1024, 2048, 4096, 8192, 16384, 32768):
+            for k in (512, 1024, 4096, 12288, 65536):
+                worst = max(worst, f(m, n, k))
+    assert 0 < worst <= limit
+    assert f(256, 4096, 12288) == limit          # the Qwen3-8B decode down projection fills it
 
 
 def test_grouped_gemm_argument_errors(lib):
