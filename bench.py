@@ -8,9 +8,12 @@ on the Qwen3-8B-shaped prefill gate_up linear (M=8192 tokens, K=4096, N=24576),
 with 1% outlier activation channels (x50) and 0.1% outlier weights (x20).
 
 The JSON line's `value` is the step's effective GEMM throughput (2MNK per step
-/ step time, TFLOP/s, all three kernels inside the timed region).  `roofline`
-is the GEMM kernel alone, timed with HIP events on the stream it runs on.
-`extra` carries the same run's weight-resync figure (36 Qwen3-8B layers, 144
+/ step time, TFLOP/s, all three kernels inside the timed region; 250 steps by
+default, about 0.2 s, with the median and minimum of the per-step times beside
+the mean).  `roofline` is the GEMM kernel alone, timed with HIP events on the
+stream it runs on (mean, median and minimum launch).
+`extra` carries the tiny configuration's step latency (64 x 512 x 512), the
+same run's weight-resync figure (36 Qwen3-8B layers, 144
 matrices, GB/s vs HBM), the MoE grouped GEMM (Qwen3-30B-A3B experts), the
 decode linears of 36 distinct Qwen3-8B layers (M=256, weights from HBM), the
 whole FP8 Qwen3-8B MLP (with the same MLP in bf16 through torch beside it) and
@@ -19,7 +22,7 @@ FP8 MFMA loop with its clock.
 `cpu_baseline` times the CPU oracle on a bounded row sample of the same step.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
-                       [--workload prefill|requant|moe|decode|mlp|moe_block|ue8m0|tis|kv|copy]
+                       [--workload prefill|tiny|requant|moe|decode|mlp|moe_block|ue8m0|tis|kv|copy]
                        [--no-cpu-baseline] [--no-extra]
 """
 import argparse
@@ -43,10 +46,10 @@ METRIC = "blockwise FP8 GEMM TFLOP/s (% FP8 MFMA peak); weight requant GB/s (% H
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=250)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="prefill", choices=["prefill", "decode", "requant", "moe", "copy", "mlp",
-                                                              "moe_block", "ue8m0", "tis", "kv"])
+    ap.add_argument("--workload", default="prefill", choices=["prefill", "tiny", "decode", "requant", "moe", "copy",
+                                                              "mlp", "moe_block", "ue8m0", "tis", "kv"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -76,30 +79,49 @@ class KernelTimer:
                     timer.pending.append((name, self.e0, self.e1))
         return _S()
 
-    def averages_ms(self):
+    def samples_ms(self):
         torch.cuda.synchronize()
         acc = {}
         for name, e0, e1 in self.pending:
             acc.setdefault(name, []).append(e0.elapsed_time(e1))
-        return {k: sum(v) / len(v) for k, v in acc.items()}
+        return acc
+
+    def averages_ms(self):
+        return {k: sum(v) / len(v) for k, v in self.samples_ms().items()}
 
 
-def timed_loop(step, steps, warmup, timer):
+def timed_loop(step, steps, warmup, timer, per_step=None):
+    """Run `warmup` untimed steps, then time exactly `steps` steps between two events.
+    Returns (mean ms per step, wall seconds); with per_step a list, each step's own
+    event-timed duration (ms) is appended to it."""
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     timer.on = True
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)] if per_step is not None else None
     t0 = time.perf_counter()
     start.record()
-    for _ in range(steps):
+    for i in range(steps):
+        if marks:
+            marks[i].record()
         step()
+    if marks:
+        marks[steps].record()
     stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     timer.on = False
+    if marks:
+        per_step.extend(marks[i].elapsed_time(marks[i + 1]) for i in range(steps))
     return start.elapsed_time(stop) / steps, wall
+
+
+def median(xs):
+    ys = sorted(xs)
+    n = len(ys)
+    return ys[n // 2] if n % 2 else 0.5 * (ys[n // 2 - 1] + ys[n // 2])
 
 
 # ---------------------------------------------------------------------------
@@ -123,17 +145,22 @@ def prefill(args, fp8rl):
         with timer.span("gemm"):
             fp8rl.fp8rl_gemm_w8a8_block(qa, sa, qw, sw, y=y)
 
-    ms, wall = timed_loop(step, args.steps, args.warmup, timer)
-    kern = timer.averages_ms()
+    per_step = []
+    ms, wall = timed_loop(step, args.steps, args.warmup, timer, per_step)
+    samples = timer.samples_ms()
+    kern = {kk: sum(v) / len(v) for kk, v in samples.items()}
     flops = 2.0 * m * n * k
     gemm_tflops = flops / (kern["gemm"] * 1e-3) / 1e12
     qw_bytes = n * k * 2 + n * k + (n // 128) * (k // 128) * 4
     qa_bytes = m * k * 2 + m * k + (k // 128) * m * 4
+    prof = gemm_profile_figures()
     out = {
         "metric": METRIC,
         "value": round(flops / (ms * 1e-3) / 1e12, 2),
         "unit": "TFLOP/s",
         "ms_per_step": round(ms, 4),
+        "ms_per_step_median": round(median(per_step), 4),
+        "ms_per_step_min": round(min(per_step), 4),
         "wall_s_timed": round(wall, 3),
         "dtype": "fp8e4m3 x fp8e4m3 -> fp32 acc -> bf16",
         "config": {"workload": "Qwen3-8B prefill gate_up linear: weight requant + activation quant + "
@@ -141,9 +168,16 @@ def prefill(args, fp8rl):
                    "weight_block": [128, 128], "act_group": [1, 128], "seed": args.seed},
         "roofline": {
             "bound": "mfma", "achieved": round(gemm_tflops, 2), "peak": FP8_PEAK_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": gemm_traffic_bytes(),
+            "unit": "TFLOP/s", "frac": round(gemm_tflops / FP8_PEAK_TFLOPS, 4), "traffic": prof["traffic"],
             "kernel": "gemm_w8a8_block", "avg_ms": round(kern["gemm"], 5),
-            "algorithmic_flops_per_launch": flops, "traffic_unit": "HBM bytes per launch",
+            "median_ms": round(median(samples["gemm"]), 5), "min_ms": round(min(samples["gemm"]), 5),
+            "launches_timed": len(samples["gemm"]),
+            "algorithmic_flops_per_launch": flops,
+            "traffic_unit": "bytes per launch crossing the L2-to-fabric boundary (rocprofv3 FETCH_SIZE + "
+                            "WRITE_SIZE, calibrated on a device copy); the memory-side cache serves part of them",
+            "sclk_GHz": prof["sclk_GHz"],
+            "sclk_source": "GRBM_GUI_ACTIVE cycles per XCD over the dispatch duration, from the committed "
+                           "counter profile of this kernel (null when the GEMM sources changed since)",
         },
         "kernels": {
             "quant_weight_block128": {"avg_ms": round(kern["quant_weight"], 5),
@@ -187,6 +221,57 @@ def prefill_ue8m0(args, fp8rl, steps=10, warmup=3):
     del a, w, qw, qa, y
     torch.cuda.empty_cache()
     return res
+
+
+# ---------------------------------------------------------------------------
+# the tiny configuration (64 x 512 x 512): latency of the whole step
+# ---------------------------------------------------------------------------
+def tiny(args, fp8rl, min_ms=250.0):
+    """The whole step on the tiny linear (M=64, K=512, N=512): weight requant,
+    activation quant and GEMM, three launches; steps are timed one by one over at
+    least min_ms and reported as median and minimum (a latency, not a throughput)."""
+    a, w = synth.tiny_linear(device="cuda")
+    m, k = a.shape
+    n = w.shape[0]
+    qw = torch.empty((n, k), dtype=torch.uint8, device="cuda")
+    sw = torch.empty((n // 128, k // 128), dtype=torch.float32, device="cuda")
+    qa = torch.empty((m, k), dtype=torch.uint8, device="cuda")
+    sa = torch.empty((k // 128, m), dtype=torch.float32, device="cuda")
+    y = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+
+    def step():
+        fp8rl.fp8rl_quant_weight_block128(w, q=qw, scale=sw)
+        fp8rl.fp8rl_quant_act_token_group128(a, q=qa, scale=sa)
+        fp8rl.fp8rl_gemm_w8a8_block(qa, sa, qw, sw, y=y)
+
+    per_step = []
+    total = 0.0
+    while total < min_ms:
+        ms, _ = timed_loop(step, 500, 20 if not per_step else 0, KernelTimer(), per_step)
+        total += ms * 500
+    # the same three launches replayed from a HIP graph: the GPU-side latency
+    # without the host's per-launch cost
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        step()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            step()
+    torch.cuda.current_stream().wait_stream(side)
+    per_replay = []
+    total = 0.0
+    while total < min_ms:
+        ms, _ = timed_loop(graph.replay, 500, 20 if not per_replay else 0, KernelTimer(), per_replay)
+        total += ms * 500
+    del graph
+    return {"workload": f"tiny blockwise W8A8 linear, M={m} K={k} N={n}: requant + quant + GEMM (3 launches)",
+            "steps_timed": len(per_step), "us_per_step_median": round(median(per_step) * 1e3, 2),
+            "us_per_step_min": round(min(per_step) * 1e3, 2),
+            "graph_replays_timed": len(per_replay), "us_per_graph_replay_median": round(median(per_replay) * 1e3, 2),
+            "us_per_graph_replay_min": round(min(per_replay) * 1e3, 2),
+            "GEMM_MFLOP": 2.0 * m * n * k / 1e6}
 
 
 # ---------------------------------------------------------------------------
@@ -304,9 +389,12 @@ def moe(args, fp8rl, steps=10, warmup=3):
         active = int((counts > 0).sum())
         nbytes = active * n * k + rows * k + rows * n * 2 + rows * (k // 128) * 4
         t = flops / (kms * 1e-3) / 1e12
+        roof_ms = max(flops / (FP8_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e3
         res[which] = {"N": n, "K": k, "rows": rows, "active_experts": active, "avg_ms": round(kms, 5),
                       "TFLOP/s": round(t, 1), "frac_fp8_peak": round(t / FP8_PEAK_TFLOPS, 4),
-                      "GB/s_min_traffic": round(nbytes / (kms * 1e-3) / 1e9, 1)}
+                      "GB/s_min_traffic": round(nbytes / (kms * 1e-3) / 1e9, 1),
+                      "min_traffic_bytes": nbytes, "roofline_ms": round(roof_ms, 5),
+                      "frac_min_roofline": round(roof_ms / kms, 4)}
     del lay
     torch.cuda.empty_cache()
     return res
@@ -663,25 +751,35 @@ def mfma_probe(blocks_per_cu=2, iters=20000):
 # ---------------------------------------------------------------------------
 GEMM_SOURCES = ["gemm_core.hpp", "gemm.hip", "common.hpp"]
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gemm_prefill_gate_up_traffic.md")
+COUNTERS_PROFILE = os.path.join(ROOT, "profiles", "gemm_prefill_gate_up_counters.md")
 
 
-def gemm_traffic_bytes():
-    """HBM bytes per GEMM launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
-    (calibrated on a device copy), read from the committed profile summary; None
-    when the GEMM sources changed since it was taken."""
+def _profile_fields(path, keys):
+    """key: value lines of a committed profile summary, or None when the GEMM
+    sources changed since it was taken (its source_sha256 line no longer matches)."""
     import hashlib
     try:
-        text = open(TRAFFIC_PROFILE).read()
+        text = open(path).read()
     except OSError:
         return None
     h = hashlib.sha256()
     for f in GEMM_SOURCES:
         with open(os.path.join(ROOT, "paper_2601_18150_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
-    fields = dict(ln.split(":", 1) for ln in text.splitlines() if ln.startswith(("hbm_bytes_per_launch:", "source_sha256:")))
+    fields = dict(ln.split(":", 1) for ln in text.splitlines() if ln.startswith(tuple(k + ":" for k in keys)))
     if fields.get("source_sha256", "").strip() != h.hexdigest()[:16]:
         return None
-    return int(fields["hbm_bytes_per_launch"].strip())
+    return {k: v.strip() for k, v in fields.items()}
+
+
+def gemm_profile_figures():
+    """HBM-side bytes per GEMM launch (rocprofv3 FETCH_SIZE / WRITE_SIZE, calibrated on
+    a device copy) and the engine clock during the GEMM (GRBM_GUI_ACTIVE), each read
+    from its committed profile summary; None where the GEMM sources changed since."""
+    tr = _profile_fields(TRAFFIC_PROFILE, ("hbm_bytes_per_launch", "source_sha256"))
+    ck = _profile_fields(COUNTERS_PROFILE, ("sclk_GHz", "source_sha256"))
+    return {"traffic": int(tr["hbm_bytes_per_launch"]) if tr and "hbm_bytes_per_launch" in tr else None,
+            "sclk_GHz": float(ck["sclk_GHz"]) if ck and "sclk_GHz" in ck else None}
 
 
 def cpu_baseline(a, w, chunk=1024, min_seconds=10.0):
@@ -690,11 +788,12 @@ def cpu_baseline(a, w, chunk=1024, min_seconds=10.0):
     min_seconds have passed or all rows are done (the sample is stated)."""
     import numpy as np
     from oracle import gemm, quant
+    cores = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
+        blas_threads = None
     m, k = a.shape
     n = w.shape[0]
     w_h = w.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
@@ -709,7 +808,8 @@ def cpu_baseline(a, w, chunk=1024, min_seconds=10.0):
         rows = r1
     dt = time.perf_counter() - t0
     flops = 2.0 * rows * n * k
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "blas_threads": blas_threads,
+            "kind": "oracle",
             "sample": f"first {rows} of {m} token rows through the full step (weight quantisation of all "
                       f"{n}x{k} weights once, activation quantisation, fp64 GEMM in {chunk}-row chunks until "
                       f"{min_seconds:.0f} s had passed); {dt:.1f} s on the host",
@@ -730,7 +830,7 @@ def main():
             print(json.dumps({"workload": "device-to-device copy of 4 GiB (torch copy_)",
                               "GB/s": hbm_copy_reference()}), flush=True)
             return
-        fn = {"requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block,
+        fn = {"tiny": tiny, "requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block,
               "ue8m0": prefill_ue8m0, "tis": tis_step, "kv": kv_decode}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
@@ -738,7 +838,7 @@ def main():
     out.update({"n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,
                 "scaling": "weak", "vs_baseline": None, "data": "synthetic"})
     if not args.no_extra:
-        extra = {"weight_resync": requant(args, fp8rl), "moe_grouped": moe(args, fp8rl),
+        extra = {"tiny": tiny(args, fp8rl), "weight_resync": requant(args, fp8rl), "moe_grouped": moe(args, fp8rl),
                  "decode_36_layers": decode(args, fp8rl), "prefill_ue8m0": prefill_ue8m0(args, fp8rl),
                  "dense_mlp": mlp(args, fp8rl),
                  "moe_block": moe_block(args, fp8rl), "tis": tis_step(args, fp8rl),
