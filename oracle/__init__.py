@@ -27,7 +27,8 @@ This package is a plain, slow, obviously-correct restatement of what the paper
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import, call or execute anything in this package.  The HIP
 product path never does; it shares no code, table or constant generator with
-this package.  Everything here is numpy on the CPU (plus one small C file,
-``e4m3_sweep.c``, used only by the exhaustive element-map test).
+this package.  Everything here is numpy on the CPU, plus one small C file,
+``quant_ref.c`` (loaded through ``cref``), a restatement of the quantisers that
+the full-size and exhaustive element-map tests use for speed.
 """
 from . import e4m3, quant, gemm, act, ue8m0, tis, kv  # noqa: F401

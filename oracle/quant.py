@@ -1,8 +1,8 @@
 """Blockwise / groupwise FP8 quantisation -- oracle, test infrastructure only.
 
-Paper section 2.1.1, Eq. (1): W_hat_ij = round(W_ij / scale_ij) in FP8, where
-scale_ij is derived from the maximum absolute value of the 128x128 block the
-element lies in.  Weights use 128x128 blocks; activations use 1x128 groups per
+Section 2.1.1, Eq. (1): each code is the FP8 rounding of the element divided by
+its block's scale, and the scale comes from the block's largest magnitude
+(readings below).  Weights use 128x128 blocks; activations use 1x128 groups per
 token, computed dynamically at every forward pass (section 2.1.1 "Static vs
 dynamic quantization"; section 3.1 names the 1x128 / 128x128 tiling).  Scales
 are fp32 (section 2.4.3 adopts FP32 scaling factors as the default).

@@ -383,3 +383,27 @@ def test_binding_rejects_cpu_tensors():
     w = torch.zeros(128, 128, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         fp8rl.fp8rl_quant_weight_block128(w)
+
+
+def test_argument_validation_under_address_and_ub_sanitizers(tmp_path):
+    """The C ABI's validation paths built for the host with AddressSanitizer and
+    UndefinedBehaviorSanitizer (tests/host/abi_asan.cpp: csrc/api.cpp with stub
+    launchers): every invalid call returns its status without launching, every
+    valid one launches once, and the sanitizers report nothing."""
+    import shutil
+    gxx = shutil.which("g++")
+    if gxx is None:
+        pytest.skip("g++ not available")
+    exe = tmp_path / "abi_asan"
+    src = os.path.join(ROOT, "tests", "host", "abi_asan.cpp")
+    build = subprocess.run([gxx, "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                            "-fno-sanitize-recover=all", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                            f"-I{os.path.join(ROOT, 'include')}", src, "-o", str(exe)],
+                           capture_output=True, text=True)
+    if build.returncode != 0 and "asan" in (build.stderr or "").lower():
+        pytest.skip("sanitizer runtime not available: " + build.stderr[-200:])
+    assert build.returncode == 0, build.stderr[-2000:]
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:verify_asan_link_order=0", UBSAN_OPTIONS="print_stacktrace=1")
+    run = subprocess.run([str(exe)], capture_output=True, text=True, env=env, timeout=120)
+    assert run.returncode == 0, run.stdout[-2000:] + run.stderr[-2000:]
+    assert run.stdout.startswith("ok"), run.stdout
