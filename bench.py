@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=250)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="prefill", choices=["prefill", "tiny", "decode", "requant", "moe", "copy",
-                                                              "mlp", "moe_block", "ue8m0", "tis", "kv"])
+                                                              "mlp", "moe_block", "ue8m0", "tis", "kv", "dma"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -357,6 +357,53 @@ def hbm_copy_reference(nbytes=4 << 30, steps=5):
     del src, dst
     torch.cuda.empty_cache()
     return round(2 * nbytes / (ms * 1e-3) / 1e9, 1)
+
+
+def dma_probe(args, fp8rl, region_kib=(16, 64, 256, 2048), waves=(4, 8, 16), inflight=(2, 8)):
+    """Rate of the global-to-LDS DMA alone (libfp8rl_probe.so), and of the same
+    16-byte loads into registers, one workgroup per CU, each streaming its own
+    region: regions of 16 KiB stay in the CU's L1, of 64 KiB (16 MiB over all
+    CUs) in the L2s, of 256 KiB in the memory-side cache, of 2 MiB (512 MiB) in
+    HBM.  Per CU: bytes per shader clock."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2601_18150_amd", "libfp8rl_probe.so"))
+    fn = lib.fp8rl_probe_dma_rate
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                   ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    blocks = torch.cuda.get_device_properties(0).multi_processor_count
+    src_bytes = blocks * max(region_kib) * 1024
+    src = torch.ones(src_bytes, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(blocks * 16 * 64, dtype=torch.float32, device="cuda")
+    clk = torch.zeros(2 * blocks, dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    rows = []
+    for to_lds, rk, w, n in ((d, r, w, n) for d in (1, 0) for r in region_kib for w in waves for n in inflight):
+        per_iter = blocks * w * n * 1024
+        iters = max(4, (1 << 30) // per_iter)           # about 1 GiB per run
+        call = (src.data_ptr(), src_bytes, rk * 1024, blocks, w, n, to_lds, iters, sink.data_ptr(),
+                clk.data_ptr(), stream)
+        if fn(*call) != 0:
+            raise RuntimeError("DMA probe launch failed")
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn(*call)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        c = clk.view(blocks, 2).double()
+        ghz = (c[:, 0].sum() / c[:, 1].sum()).item() * 0.1
+        moved = per_iter * iters
+        rows.append({"into": "LDS" if to_lds else "registers", "region_KiB": rk, "waves": w, "inflight": n,
+                     "TB/s": round(moved / (ms * 1e-3) / 1e12, 3),
+                     "B_per_clk_per_CU": round(moved / blocks / (ms * 1e-3 * ghz * 1e9), 2),
+                     "clock_GHz": round(ghz, 3)})
+    del src, sink
+    torch.cuda.empty_cache()
+    return {"workload": f"global-to-LDS DMA and register loads alone, {blocks} workgroups (one per CU), 16 bytes "
+                        f"per lane",
+            "rows": rows}
 
 
 # ---------------------------------------------------------------------------
@@ -831,7 +878,7 @@ def main():
                               "GB/s": hbm_copy_reference()}), flush=True)
             return
         fn = {"tiny": tiny, "requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block,
-              "ue8m0": prefill_ue8m0, "tis": tis_step, "kv": kv_decode}[args.workload]
+              "ue8m0": prefill_ue8m0, "tis": tis_step, "kv": kv_decode, "dma": dma_probe}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
     out, (a, w) = prefill(args, fp8rl)

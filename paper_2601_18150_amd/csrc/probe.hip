@@ -9,7 +9,10 @@
 //    its error can be measured against the exact value for every input;
 //  * single v_mfma_f32_16x16x128_f8f6f4 instructions on operands given by the
 //    host, so that the instruction's summation of its 128 products (and of the
-//    accumulator input) can be compared with the exact sums.
+//    accumulator input) can be compared with the exact sums;
+//  * the global-to-LDS DMA the GEMMs feed their operand tiles with, alone (no
+//    compute), streaming regions of chosen sizes, so that the rate one CU can
+//    pull from L1-, L2- or HBM-resident data is measured directly.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -44,6 +47,55 @@ __global__ __launch_bounds__(256) void mfma_rate_kernel(float* __restrict__ out,
   float acc = 0.f;
   for (int i = 0; i < 4; ++i) acc += c0[i] + c1[i] + c2[i] + c3[i];
   out[blockIdx.x * 256 + t] = acc;
+  if (t == 0) {
+    clk[2 * blockIdx.x] = s1 - s0;
+    clk[2 * blockIdx.x + 1] = r1 - r0;
+  }
+}
+
+// Workgroup b streams region b of src ([b * region, (b + 1) * region)) into LDS
+// with 16-byte-per-lane DMA instructions (1 KiB per wave instruction, as the
+// GEMM K loop issues them), or (kToLds false) into registers with the same
+// 16-byte loads: each wave issues kInflight instructions, waits for
+// them, and moves on, `iters` rounds, walking the region's 1 KiB chunks
+// cyclically.  The buffer resource spans exactly the region, so an offset past
+// it would read zeros rather than leave it (the host also checks the regions
+// fit in src).  clk[2b], clk[2b+1]: shader-clock and 100 MHz real-time ticks.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+template <int kInflight, bool kToLds>
+__global__ __launch_bounds__(1024) void dma_rate_kernel(const uint8_t* __restrict__ src, uint32_t region, int iters,
+                                                        float* __restrict__ sink, unsigned long long* __restrict__ clk) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[64 * 1024];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int waves = blockDim.x >> 6;
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(src + (int64_t)blockIdx.x * region), (short)0, (int)region, 0x00020000);
+  const uint32_t chunks = region >> 10;
+  uint32_t c = (uint32_t)(wave * kInflight) % chunks;          // every offset below stays < region
+  const uint32_t step = (uint32_t)(waves * kInflight) % chunks;
+  uint32_t x = 0;
+  const unsigned long long s0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < kInflight; ++i) {
+      const uint32_t ci = (c + i) % chunks;
+      if constexpr (kToLds) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)(lds + ((wave * kInflight + i) & 63) * 1024), 16,
+                                                 (ci << 10) + lane * 16, 0, 0, 0);
+      } else {
+        const v4u32 v = __builtin_amdgcn_raw_buffer_load_b128(r, (ci << 10) + lane * 16, 0, 0);
+        x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);    // vmcnt(0)
+    c = (c + step) % chunks;
+  }
+  const unsigned long long s1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+  __syncthreads();
+  sink[(int64_t)blockIdx.x * blockDim.x + t] = (float)lds[(t * 16) & (64 * 1024 - 1)] + (float)x;
   if (t == 0) {
     clk[2 * blockIdx.x] = s1 - s0;
     clk[2 * blockIdx.x + 1] = r1 - r0;
@@ -113,4 +165,35 @@ extern "C" int fp8rl_probe_silu_fast(const uint16_t* g, const uint16_t* u, float
   hipLaunchKernelGGL(silu_fast_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
                      static_cast<hipStream_t>(stream), g, u, r, q, (int64_t)n);
   return hipGetLastError() == hipSuccess ? 0 : 4;
+}
+
+// DMA-rate probe.  src: src_bytes of device memory; region: bytes streamed by
+// each workgroup, a multiple of 1024 below 2^31, blocks * region <= src_bytes;
+// waves: 1..16 per workgroup; inflight: 1, 2, 4 or 8 instructions per wave
+// between waits; to_lds: 1 for the DMA into LDS, 0 for loads into registers; sink: blocks * waves * 64 floats; clk: 2 * blocks.  Moves
+// iters * blocks * waves * inflight KiB.  0 on success, 1 on a bad argument,
+// 4 on a launch failure.
+extern "C" int fp8rl_probe_dma_rate(const uint8_t* src, long long src_bytes, long long region, int blocks, int waves,
+                                    int inflight, int to_lds, int iters, float* sink, unsigned long long* clk,
+                                    void* stream) {
+  if (!src || !sink || !clk || blocks < 1 || waves < 1 || waves > 16 || iters < 1) return 1;
+  if (region < 1024 || region % 1024 || region >= (1ll << 31) || src_bytes < 0 || (long long)blocks > src_bytes / region)
+    return 1;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const dim3 grid((unsigned)blocks), block((unsigned)(64 * waves));
+  const uint32_t reg = (uint32_t)region;
+#define FP8RL_DMA(N)                                                                                            \
+  if (inflight == N) {                                                                                          \
+    if (to_lds)                                                                                                 \
+      hipLaunchKernelGGL((dma_rate_kernel<N, true>), grid, block, 0, st, src, reg, iters, sink, clk);           \
+    else                                                                                                        \
+      hipLaunchKernelGGL((dma_rate_kernel<N, false>), grid, block, 0, st, src, reg, iters, sink, clk);          \
+    return hipGetLastError() == hipSuccess ? 0 : 4;                                                             \
+  }
+  FP8RL_DMA(1)
+  FP8RL_DMA(2)
+  FP8RL_DMA(4)
+  FP8RL_DMA(8)
+#undef FP8RL_DMA
+  return 1;
 }

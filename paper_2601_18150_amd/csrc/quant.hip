@@ -206,53 +206,43 @@ __global__ __launch_bounds__(256) void quant_act_token_group128_kernel(
 // ---------------------------------------------------------------------------
 // Down-projection input of the gated MLP: h = bf16(SiLU(gate) * up) from the
 // fused gate_up output [gate | up] (silu_math.hpp: correctly rounded), then the
-// same 1x128 group quantisation.  Lane mapping as the activation kernel: 16
-// lanes per (token, group), each lane 8 elements of gate and the matching 8 of
-// up.  h is written out only when asked for.
+// same 1x128 group quantisation.  16 lanes per (token, group), each lane 8
+// elements of gate and the matching 8 of up.  A workgroup covers 16 * kUnits
+// consecutive tokens of one 128-wide group, so its scale stores (scales are
+// token-contiguous per group) fill whole cache lines inside one workgroup
+// instead of single floats scattered over many.  gate and up are read once:
+// streaming loads.  h is written out only when asked for.
 // ---------------------------------------------------------------------------
 template <int kUnits>
 __global__ __launch_bounds__(256) void silu_mul_quant_group128_kernel(
     const uint16_t* __restrict__ gu, int64_t ld_gu, int64_t inter, uint8_t* __restrict__ q, int64_t ldq,
-    float* __restrict__ scale, int64_t ld_scale, uint16_t* __restrict__ h, int64_t ldh, uint32_t units, uint32_t ng) {
+    float* __restrict__ scale, int64_t ld_scale, uint16_t* __restrict__ h, int64_t ldh, uint32_t m, uint32_t ng) {
   const int t = threadIdx.x;
   const int chunk = t & 15;
-  // The workgroup covers 16 * kUnits consecutive units; lane row j = t / 16 takes
-  // units unit0 + 16 k + j.  (row, group) of unit0 in scalar registers, then at
-  // most 16 / ng + 1 steps per unit (units < 2^28, checked by the caller).
-  const uint32_t unit0 = blockIdx.x * (16u * kUnits);
-  const uint32_t row0 = unit0 / ng;
-  uint32_t gg = unit0 - row0 * ng + (t >> 4);
-  uint32_t rr = row0;
-  int64_t row[kUnits];
-  int grp[kUnits];
+  const uint32_t rb = blockIdx.x / ng;            // block of 16 * kUnits tokens
+  const uint32_t g = blockIdx.x - rb * ng;        // 128-wide group
+  uint32_t row[kUnits];
   bool valid[kUnits];
   uint4 vg[kUnits], vu[kUnits];
 #pragma unroll
   for (int k = 0; k < kUnits; ++k) {
-    if (k) gg += 16;
-    while (gg >= ng) {
-      gg -= ng;
-      ++rr;
-    }
-    const uint32_t unit = unit0 + 16u * k + (t >> 4);
-    valid[k] = unit < units;
-    // an out-of-range unit re-reads the last unit (every lane stays in bounds)
-    row[k] = valid[k] ? (int64_t)rr : (int64_t)((units - 1) / ng);
-    grp[k] = valid[k] ? (int)gg : (int)((units - 1) % ng);
-    const uint16_t* src = gu + row[k] * ld_gu + grp[k] * 128 + chunk * 8;
-    vg[k] = *reinterpret_cast<const uint4*>(src);
-    vu[k] = *reinterpret_cast<const uint4*>(src + inter);
+    const uint32_t r = rb * (16u * kUnits) + 16u * k + (t >> 4);
+    valid[k] = r < m;
+    row[k] = valid[k] ? r : m - 1;                // rows past the end re-read the last row (in bounds)
+    const uint16_t* src = gu + (int64_t)row[k] * ld_gu + g * 128 + chunk * 8;
+    vg[k] = load_stream16(src);
+    vu[k] = load_stream16(src + inter);
   }
 #pragma unroll
   for (int k = 0; k < kUnits; ++k) {
     const uint4 v = silu::silu_mul8(vg[k], vu[k]);
-    const uint32_t m = row16_max(amax16_of(v));
-    const BlockScale bs = qmath::block_scale(m);
+    const uint32_t mx = row16_max(amax16_of(v));
+    const BlockScale bs = qmath::block_scale(mx);
     const uint2 c = quant8_block<false>(v, bs);
     if (valid[k]) {
-      *reinterpret_cast<uint2*>(q + row[k] * ldq + grp[k] * 128 + chunk * 8) = c;
-      if (chunk == 0) scale[(int64_t)grp[k] * ld_scale + row[k]] = bs.scale;
-      if (h) *reinterpret_cast<uint4*>(h + row[k] * ldh + grp[k] * 128 + chunk * 8) = v;
+      *reinterpret_cast<uint2*>(q + (int64_t)row[k] * ldq + g * 128 + chunk * 8) = c;
+      if (chunk == 0) scale[(int64_t)g * ld_scale + row[k]] = bs.scale;
+      if (h) *reinterpret_cast<uint4*>(h + (int64_t)row[k] * ldh + g * 128 + chunk * 8) = v;
     }
   }
 }
@@ -283,12 +273,23 @@ __global__ __launch_bounds__(256) void gather_rows_fp8_kernel(
 hipError_t launch_silu_mul_quant_group128(const uint16_t* gu, int64_t m, int64_t inter, int64_t ld_gu,
                                           uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
                                           uint16_t* h, int64_t ldh, hipStream_t stream) {
-  const uint32_t ng = (uint32_t)(inter / 128);
-  const uint32_t units = (uint32_t)(m * ng);          // < 2^28
-  constexpr int kUnits = 2;   // measured: 1 unit per lane 8% slower, 4 units 2% slower
-  const uint32_t blocks = (units + 16 * kUnits - 1) / (16 * kUnits);
-  hipLaunchKernelGGL(silu_mul_quant_group128_kernel<kUnits>, dim3(blocks), dim3(256), 0, stream, gu, ld_gu,
-                     inter, q, ldq, scale, ld_scale, h, ldh, units, ng);
+  const uint32_t ng = (uint32_t)(inter / 128);      // m * ng < 2^28 (checked by the caller)
+  // tokens per workgroup: 64 while that still gives 2048 workgroups (eight per
+  // CU), else 32, else 16.  Measured (us, 8192 x 12288 / 32768 x 768 / 256 x
+  // 12288): 64 tokens 93.5 / 29.9 / 9.8, 32 tokens 97.5 / 30.6 / 8.6, 16 tokens
+  // 96.9 / 30.6 / 7.9; 128 tokens 103.5 at the first shape.
+  const auto blocks_for = [&](int64_t tokens) { return (uint32_t)((m + tokens - 1) / tokens) * ng; };
+  constexpr uint32_t kMinBlocks = 2048;
+  const uint32_t b4 = blocks_for(64), b2 = blocks_for(32), b1 = blocks_for(16);
+  if (b4 >= kMinBlocks)
+    hipLaunchKernelGGL(silu_mul_quant_group128_kernel<4>, dim3(b4), dim3(256), 0, stream, gu, ld_gu, inter, q, ldq,
+                       scale, ld_scale, h, ldh, (uint32_t)m, ng);
+  else if (b2 >= kMinBlocks)
+    hipLaunchKernelGGL(silu_mul_quant_group128_kernel<2>, dim3(b2), dim3(256), 0, stream, gu, ld_gu, inter, q, ldq,
+                       scale, ld_scale, h, ldh, (uint32_t)m, ng);
+  else
+    hipLaunchKernelGGL(silu_mul_quant_group128_kernel<1>, dim3(b1), dim3(256), 0, stream, gu, ld_gu, inter, q, ldq,
+                       scale, ld_scale, h, ldh, (uint32_t)m, ng);
   return hipGetLastError();
 }
 

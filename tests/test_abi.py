@@ -377,6 +377,27 @@ def test_attention_decode_argument_errors(lib):
     assert g(A16, A16, A16, 10, A16, 8, A16, 2, 8, 2, 128, 100, 0.088, A16, None, ws, None) == INVALID
 
 
+def test_dma_probe_rejects_regions_outside_the_buffer():
+    """The operand-stream probe checks on the host that every workgroup's region
+    lies inside the source buffer (and its other sizes) before launching."""
+    import paper_2601_18150_amd as fp8rl
+    probe = ctypes.CDLL(os.path.join(os.path.dirname(fp8rl.LIB_PATH), "libfp8rl_probe.so"))
+    fn = probe.fp8rl_probe_dma_rate
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_longlong, ctypes.c_longlong, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                   ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    good = dict(src=A16, src_bytes=1 << 30, region=1 << 20, blocks=256, waves=8, inflight=8, to_lds=1, iters=4,
+                sink=A16, clk=A16)
+    bad = [dict(src_bytes=(1 << 28) - 1),        # 256 regions of 1 MiB need 256 MiB
+           dict(region=1000), dict(region=512), dict(region=1 << 31), dict(blocks=0), dict(waves=0),
+           dict(waves=17), dict(inflight=3), dict(inflight=16), dict(iters=0), dict(src=None), dict(sink=None),
+           dict(clk=None), dict(src_bytes=-1)]
+    for b in bad:
+        a = dict(good, **b)
+        assert fn(a["src"], a["src_bytes"], a["region"], a["blocks"], a["waves"], a["inflight"], a["to_lds"],
+                  a["iters"], a["sink"], a["clk"], None) == 1, b
+
+
 def test_binding_rejects_cpu_tensors():
     import torch
     import paper_2601_18150_amd as fp8rl
