@@ -178,24 +178,26 @@ __global__ __launch_bounds__(256) void quant_weight_block128_batched_kernel(cons
 
 // ---------------------------------------------------------------------------
 // Activation: 16 lanes per (token, group); a 256-thread workgroup covers 16
-// consecutive (token, group) units in row-major order, so a wave reads 1 KiB of
-// contiguous row data when the four units share a token.
+// consecutive tokens of one 128-wide group, so its 16 scale stores (scales are
+// token-contiguous per group) are one 64-byte run instead of 16 floats ld_scale
+// apart.  Plain (cached) loads: the activations usually come straight from the
+// previous kernel and still sit in the memory-side cache.
 // ---------------------------------------------------------------------------
 template <bool kPow2Scale>
 __global__ __launch_bounds__(256) void quant_act_token_group128_kernel(
     const uint16_t* __restrict__ a, int64_t lda, uint8_t* __restrict__ q, int64_t ldq,
-    float* __restrict__ scale, int64_t ld_scale, int64_t units, int ng) {
+    float* __restrict__ scale, int64_t ld_scale, uint32_t m, uint32_t ng) {
   const int t = threadIdx.x;
-  const int64_t unit = (int64_t)blockIdx.x * 16 + (t >> 4);
-  const bool valid = unit < units;
-  const int64_t u = valid ? unit : units - 1;      // keep every lane in bounds
-  const int64_t row = u / ng;
-  const int g = (int)(u - row * ng);
   const int chunk = t & 15;
+  const uint32_t rb = blockIdx.x / ng;             // block of 16 tokens
+  const uint32_t g = blockIdx.x - rb * ng;         // 128-wide group
+  const uint32_t r = rb * 16u + (uint32_t)(t >> 4);
+  const bool valid = r < m;
+  const int64_t row = valid ? r : m - 1;           // rows past the end re-read the last row (in bounds)
 
   const uint4 v = *reinterpret_cast<const uint4*>(a + row * lda + g * 128 + chunk * 8);
-  const uint32_t m = row16_max(amax16_of(v));
-  const BlockScale bs = scale_of<kPow2Scale>(m);
+  const uint32_t mx = row16_max(amax16_of(v));
+  const BlockScale bs = scale_of<kPow2Scale>(mx);
   const uint2 c = quant8_block<kPow2Scale>(v, bs);
   if (valid) {
     *reinterpret_cast<uint2*>(q + row * ldq + g * 128 + chunk * 8) = c;
@@ -343,15 +345,19 @@ hipError_t launch_quant_weight_block128_batched(const WeightJob* jobs, int count
 hipError_t launch_quant_act_token_group128(const uint16_t* a, int64_t m, int64_t k, int64_t lda,
                                            uint8_t* q, int64_t ldq, float* scale, int64_t ld_scale,
                                            hipStream_t stream, bool pow2_scale) {
-  const int ng = (int)(k / 128);
-  const int64_t units = m * ng;
-  const int64_t blocks = (units + 15) / 16;
+  // m * (k / 128) < 2^28 (checked by the caller), so the grid fits 32 bits.  Measured
+  // on 8192 x 4096 inside the prefill step (weight requant, this, GEMM): 20.7 us,
+  // against 22.0 us for workgroups over 16 consecutive (token, group) units in
+  // row-major order, and 24.6 / 27.8 us with streaming loads (which pay off only
+  // when the input is not in any cache: 24.1 vs 32.8 us after a cache flush).
+  const uint32_t ng = (uint32_t)(k / 128);
+  const uint32_t blocks = (uint32_t)((m + 15) / 16) * ng;
   if (pow2_scale)
-    hipLaunchKernelGGL(quant_act_token_group128_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       a, lda, q, ldq, scale, ld_scale, units, ng);
+    hipLaunchKernelGGL(quant_act_token_group128_kernel<true>, dim3(blocks), dim3(256), 0, stream,
+                       a, lda, q, ldq, scale, ld_scale, (uint32_t)m, ng);
   else
-    hipLaunchKernelGGL(quant_act_token_group128_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                       a, lda, q, ldq, scale, ld_scale, units, ng);
+    hipLaunchKernelGGL(quant_act_token_group128_kernel<false>, dim3(blocks), dim3(256), 0, stream,
+                       a, lda, q, ldq, scale, ld_scale, (uint32_t)m, ng);
   return hipGetLastError();
 }
 
