@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=250)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="prefill", choices=["prefill", "tiny", "decode", "requant", "moe", "copy",
-                                                              "mlp", "moe_block", "ue8m0", "tis", "kv", "dma"])
+                                                              "mlp", "moe_block", "ue8m0", "tis", "kv", "dma", "loop"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true")
     ap.add_argument("--seed", type=int, default=3)
@@ -404,6 +404,47 @@ def dma_probe(args, fp8rl, region_kib=(16, 64, 256, 2048), waves=(4, 8, 16), inf
     return {"workload": f"global-to-LDS DMA and register loads alone, {blocks} workgroups (one per CU), 16 bytes "
                         f"per lane",
             "rows": rows}
+
+
+def mfma_loop_probe(args, fp8rl, iters=4000):
+    """The GEMM K step's inner loop without memory traffic (libfp8rl_probe.so):
+    fragment reads from LDS and MFMAs on the prefill's 128n x 64m and the decode /
+    MoE 64n x 64m wave tiles, 8 waves per CU, with and without the per-K-block
+    scale FMAs and the per-step barrier; TFLOP/s against the spec peak and the
+    register-fed MFMA loop of the same run (which holds a lower clock)."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2601_18150_amd", "libfp8rl_probe.so"))
+    fn = lib.fp8rl_probe_mfma_loop
+    fn.argtypes = [ctypes.c_int] * 5 + [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    blocks = torch.cuda.get_device_properties(0).multi_processor_count
+    out = torch.empty(blocks * 512, dtype=torch.float32, device="cuda")
+    clk = torch.zeros(2 * blocks, dtype=torch.int64, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    ref = mfma_probe()
+    rows = []
+    for tile, (tn, tm) in ((0, (8, 4)), (1, (4, 4))):
+        for fma in (0, 1):
+            for barrier in (0, 1):
+                call = (tile, fma, barrier, blocks, iters, out.data_ptr(), clk.data_ptr(), stream)
+                if fn(*call) != 0:
+                    raise RuntimeError("inner-loop probe launch failed")
+                torch.cuda.synchronize()
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn(*call)
+                e1.record()
+                torch.cuda.synchronize()
+                ms = e0.elapsed_time(e1)
+                c = clk.view(blocks, 2).double()
+                ghz = (c[:, 0].sum() / c[:, 1].sum()).item() * 0.1
+                flops = blocks * 8 * iters * tn * tm * 2.0 * 16 * 16 * 128
+                tf = flops / (ms * 1e-3) / 1e12
+                rows.append({"wave_tile": f"{16 * tn}n x {16 * tm}m", "scale_fma": bool(fma), "barrier": bool(barrier),
+                             "TFLOP/s": round(tf, 1), "frac_of_spec": round(tf / FP8_PEAK_TFLOPS, 4),
+                             "frac_of_mfma_loop": round(tf / ref["TFLOP/s"], 4), "clock_GHz": round(ghz, 3)})
+    return {"workload": f"GEMM K-step inner loop alone: LDS fragment reads + MFMAs, {blocks} workgroups of 8 waves",
+            "mfma_loop_reference": ref, "rows": rows}
 
 
 # ---------------------------------------------------------------------------
@@ -878,7 +919,7 @@ def main():
                               "GB/s": hbm_copy_reference()}), flush=True)
             return
         fn = {"tiny": tiny, "requant": requant, "moe": moe, "decode": decode, "mlp": mlp, "moe_block": moe_block,
-              "ue8m0": prefill_ue8m0, "tis": tis_step, "kv": kv_decode, "dma": dma_probe}[args.workload]
+              "ue8m0": prefill_ue8m0, "tis": tis_step, "kv": kv_decode, "dma": dma_probe, "loop": mfma_loop_probe}[args.workload]
         print(json.dumps(fn(args, fp8rl)), flush=True)
         return
     out, (a, w) = prefill(args, fp8rl)

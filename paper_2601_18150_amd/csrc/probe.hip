@@ -12,7 +12,11 @@
 //    accumulator input) can be compared with the exact sums;
 //  * the global-to-LDS DMA the GEMMs feed their operand tiles with, alone (no
 //    compute), streaming regions of chosen sizes, so that the rate one CU can
-//    pull from L1-, L2- or HBM-resident data is measured directly.
+//    pull from L1-, L2- or HBM-resident data is measured directly;
+//  * the GEMM K step's inner loop without its memory traffic: per step each of
+//    8 waves reads its wave tile's fragments from LDS and issues its MFMAs,
+//    optionally with the per-K-block scale FMAs and a workgroup barrier, so
+//    that what each costs the MFMA pipes is measured on its own.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -96,6 +100,83 @@ __global__ __launch_bounds__(1024) void dma_rate_kernel(const uint8_t* __restric
   const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
   __syncthreads();
   sink[(int64_t)blockIdx.x * blockDim.x + t] = (float)lds[(t * 16) & (64 * 1024 - 1)] + (float)x;
+  if (t == 0) {
+    clk[2 * blockIdx.x] = s1 - s0;
+    clk[2 * blockIdx.x + 1] = r1 - r0;
+  }
+}
+
+// Inner loop of one K step, 8 waves (two per SIMD), wave tile (16 TN) n x
+// (16 TM) m as the GEMMs lay it out: per step TM + TN fragments of 32 bytes per
+// lane read from LDS (two ds_read_b128 each) and TN x TM MFMAs.  kFma: MFMA
+// into a zero accumulator, then acc += p * scale (four FMAs per MFMA, as the
+// fp32-scale GEMM); else the MFMA accumulates in place.  kBarrier: s_barrier
+// after every step, as the GEMM's LDS ring needs.  The fragments are fixed
+// data; nothing is written to LDS after the start.
+typedef int v8i32p __attribute__((ext_vector_type(8)));
+typedef float v4f32p __attribute__((ext_vector_type(4)));
+template <int TN, int TM, bool kFma, bool kBarrier>
+__global__ __launch_bounds__(512) void mfma_loop_kernel(int iters, float* __restrict__ out,
+                                                        unsigned long long* __restrict__ clk) {
+  __shared__ __attribute__((aligned(16))) uint8_t lds[96 * 1024];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  for (int i = t; i < 96 * 1024 / 16; i += blockDim.x)
+    reinterpret_cast<v4u32*>(lds)[i] = (v4u32){0x38383838u + (unsigned)(i & 7), 0x3A3A3A3Au, 0x34343434u, 0x36363636u};
+  __syncthreads();
+  // wave w: n half (w & 1) of the W fragments, m quarter (w >> 1) of the A fragments
+  const int wbase = (wave & 1) * TN * 2048;                       // < 2 * 8 * 2048 = 32 KiB
+  const int abase = 32 * 1024 + (wave >> 1) * TM * 2048;          // < 32 KiB + 4 * 4 * 2048 = 64 KiB
+  const int lo = lane * 16;
+  v4f32p acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = (v4f32p){0.f, 0.f, 0.f, 0.f};
+  float sc[TM];
+#pragma unroll
+  for (int j = 0; j < TM; ++j) sc[j] = 1.0f + (float)j * 0.25f;
+  auto frag = [&](int off) {
+    const v4u32 u0 = *reinterpret_cast<const v4u32*>(lds + off + lo);
+    const v4u32 u1 = *reinterpret_cast<const v4u32*>(lds + off + 1024 + lo);
+    return (v8i32p){(int)u0[0], (int)u0[1], (int)u0[2], (int)u0[3], (int)u1[0], (int)u1[1], (int)u1[2], (int)u1[3]};
+  };
+  const unsigned long long s0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  for (int it = 0; it < iters; ++it) {
+    v8i32p bf[TM];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) bf[tm] = frag(abase + tm * 2048);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const v8i32p af = frag(wbase + tn * 2048);
+      if constexpr (kFma) {
+        v4f32p p[TM];
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+          p[tm] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf[tm], (v4f32p){0.f, 0.f, 0.f, 0.f}, 0, 0, 0,
+                                                                   0, 0, 0);
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[tn][tm][r] = __builtin_fmaf(p[tm][r], sc[tm], acc[tn][tm][r]);
+      } else {
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+          acc[tn][tm] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(af, bf[tm], acc[tn][tm], 0, 0, 0, 0, 0, 0);
+      }
+    }
+    if constexpr (kBarrier) __syncthreads();
+#pragma unroll
+    for (int j = 0; j < TM; ++j) sc[j] = sc[j] * 0.999f + 1e-7f;     // a new scale per step
+  }
+  const unsigned long long s1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+  float f = 0.f;
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) f += acc[i][j][0] + acc[i][j][3];
+  out[(int64_t)blockIdx.x * blockDim.x + t] = f;
   if (t == 0) {
     clk[2 * blockIdx.x] = s1 - s0;
     clk[2 * blockIdx.x + 1] = r1 - r0;
@@ -196,4 +277,33 @@ extern "C" int fp8rl_probe_dma_rate(const uint8_t* src, long long src_bytes, lon
   FP8RL_DMA(8)
 #undef FP8RL_DMA
   return 1;
+}
+
+// K-step inner-loop probe: blocks workgroups of 512 threads (8 waves); tile 0 =
+// wave tile 128n x 64m (the prefill GEMM's), 1 = 64n x 64m (the decode and MoE
+// tiles'); fma, barrier: 0 or 1 (see mfma_loop_kernel).  out: blocks * 512
+// floats; clk: 2 * blocks.  Each wave issues iters * TN * TM MFMAs.  0 on
+// success, 1 on a bad argument, 4 on a launch failure.
+extern "C" int fp8rl_probe_mfma_loop(int tile, int fma, int barrier, int blocks, int iters, float* out,
+                                     unsigned long long* clk, void* stream) {
+  if (!out || !clk || blocks < 1 || iters < 1 || tile < 0 || tile > 1 || fma < 0 || fma > 1 || barrier < 0 ||
+      barrier > 1)
+    return 1;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const dim3 grid((unsigned)blocks), block(512);
+#define FP8RL_LOOP(TN, TM, F, B) \
+  hipLaunchKernelGGL((mfma_loop_kernel<TN, TM, F, B>), grid, block, 0, st, iters, out, clk)
+  const int sel = tile * 4 + fma * 2 + barrier;
+  switch (sel) {
+    case 0: FP8RL_LOOP(8, 4, false, false); break;
+    case 1: FP8RL_LOOP(8, 4, false, true); break;
+    case 2: FP8RL_LOOP(8, 4, true, false); break;
+    case 3: FP8RL_LOOP(8, 4, true, true); break;
+    case 4: FP8RL_LOOP(4, 4, false, false); break;
+    case 5: FP8RL_LOOP(4, 4, false, true); break;
+    case 6: FP8RL_LOOP(4, 4, true, false); break;
+    default: FP8RL_LOOP(4, 4, true, true); break;
+  }
+#undef FP8RL_LOOP
+  return hipGetLastError() == hipSuccess ? 0 : 4;
 }
