@@ -398,6 +398,19 @@ def test_dma_probe_rejects_regions_outside_the_buffer():
                   a["iters"], a["sink"], a["clk"], None) == 1, b
 
 
+def test_inner_loop_probe_rejects_bad_arguments():
+    import paper_2601_18150_amd as fp8rl
+    probe = ctypes.CDLL(os.path.join(os.path.dirname(fp8rl.LIB_PATH), "libfp8rl_probe.so"))
+    fn = probe.fp8rl_probe_mfma_loop
+    fn.argtypes = [ctypes.c_int] * 5 + [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    good = [0, 1, 1, 256, 10, A16, A16, None]
+    for i, bad in [(0, 2), (0, -1), (1, 2), (2, 2), (3, 0), (4, 0), (5, None), (6, None)]:
+        a = list(good)
+        a[i] = bad
+        assert fn(*a) == 1, (i, bad)
+
+
 def test_binding_rejects_cpu_tensors():
     import torch
     import paper_2601_18150_amd as fp8rl
