@@ -628,7 +628,8 @@ def moe_block(args, fp8rl, steps=10, warmup=3):
 
 def tis_step(args, fp8rl, steps=20, warmup=5):
     """Token-level TIS weights and mismatch-KL sums over one rollout batch (32 prompts x
-    16 samples x 20480 tokens, padding masked), C = 2."""
+    16 samples x 20480 tokens, padding masked), C = 2: HIP events around each call,
+    and 20 calls back to back replayed from a HIP graph."""
     lt, lr, mask = synth.rollout_logprobs(device="cuda")
     n = lt.numel()
     w = torch.empty(n, dtype=torch.float32, device="cuda")
@@ -642,10 +643,29 @@ def tis_step(args, fp8rl, steps=20, warmup=5):
 
     timed_loop(step, steps, warmup, timer)
     ms = timer.averages_ms()["tis"]
+    # the same call 20 times back to back in a HIP graph: per-call time without the
+    # launch and event overhead that dominates a single 25 us call's span
+    calls = 20
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        fp8rl.fp8rl_tis_weights_kl(lt, lr, mask, 2.0, w_tis=w, stats=stats, workspace=work)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            for _ in range(calls):
+                fp8rl.fp8rl_tis_weights_kl(lt, lr, mask, 2.0, w_tis=w, stats=stats, workspace=work)
+    torch.cuda.current_stream().wait_stream(side)
+    graph_ms, _ = timed_loop(graph.replay, 10, 2, KernelTimer())
+    del graph
+    per_call = graph_ms / calls
     nbytes = n * (4 + 4 + 1 + 4)
     res = {"workload": f"TIS weights + mismatch-KL sums, {n} rollout tokens (32 x 16 x 20480)",
            "avg_ms": round(ms, 5), "bytes": nbytes, "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1),
-           "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+           "frac_hbm": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "graph_ms_per_call": round(per_call, 5),
+           "graph_GB/s": round(nbytes / (per_call * 1e-3) / 1e9, 1),
+           "graph_frac_hbm": round(nbytes / (per_call * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     del lt, lr, mask, w, work
     torch.cuda.empty_cache()
     return res
