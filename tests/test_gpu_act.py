@@ -162,9 +162,22 @@ def test_silu_mul_quant_dense_mlp_full_sampled(fp8rl):
     gu = synth.gate_up_output(seed=23, device="cuda", m=8192, inter=12288)
     q, s, h = fp8rl.fp8rl_silu_mul_quant_group128(gu, want_h=True)
     torch.cuda.synchronize()
-    rows = np.sort(np.random.default_rng(23).choice(8192, 256, replace=False))
-    rows[-1] = 8191
+    # 256 seeded rows, plus one row of every 16-row group at a varying offset, so that every
+    # workgroup (64 consecutive tokens of one group) and every lane row of it is checked
+    rng_rows = np.random.default_rng(23).choice(8192, 256, replace=False)
+    grid_rows = np.arange(0, 8192, 16) + (np.arange(512) * 5) % 16
+    rows = np.unique(np.concatenate([rng_rows, grid_rows, [8191]]))
     check_fused(gu, 12288, q, s, h, rows=rows)
+
+
+def test_silu_mul_quant_mid_size_every_row(fp8rl):
+    """1000 tokens x intermediate 12288: the launch that puts 32 tokens in a workgroup
+    (fewer than 2048 workgroups of 64), with a ragged last block; every row checked."""
+    announce("silu_mul_quant 1000 x (2 x 12288), every row")
+    gu = synth.gate_up_output(seed=24, device="cuda", m=1000, inter=12288)
+    q, s, h = fp8rl.fp8rl_silu_mul_quant_group128(gu, want_h=True)
+    torch.cuda.synchronize()
+    check_fused(gu, 12288, q, s, h)
 
 
 def test_silu_mul_quant_zero_rows_is_noop(fp8rl):
