@@ -952,7 +952,9 @@ def main():
                  "moe_block": moe_block(args, fp8rl), "tis": tis_step(args, fp8rl),
                  "kv_decode_attention": kv_decode(args, fp8rl),
                  "hbm_copy_GB/s": hbm_copy_reference(),
-                 "mfma_probe": mfma_probe()}
+                 "mfma_probe": mfma_probe(),
+                 "operand_streams": dma_probe(args, fp8rl, region_kib=(64, 2048), waves=(8,), inflight=(8,)),
+                 "k_step_inner_loop": mfma_loop_probe(args, fp8rl)}
         out["extra"] = extra
         out["roofline"]["frac_of_measured_mfma_loop"] = round(
             out["roofline"]["achieved"] / extra["mfma_probe"]["TFLOP/s"], 4)
